@@ -1,0 +1,155 @@
+#!/usr/bin/env python
+"""Benchmark of the warp-specialised GEMM on one MI355X.
+
+Metric: bf16 GEMM TFLOP/s (and fraction of the dense MFMA peak) at
+M = N = K = 8192, bf16 operands ~ N(0,1), fp32 output.  One step is one full
+C = A B.  Operands are generated once (seeded, synthetic) and are resident in
+HBM before the timed region starts.
+
+    python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--point TMxTNxTKxSxNPxNC]
+
+Prints one JSON line.  Also reported: the dominant kernel's roofline entry
+(device time per launch from HIP events on the launch stream) and the CPU
+oracle timed on this host's cores over a bounded sample of the same product.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+WORKLOAD = "gemm_8192x8192x8192_bf16_normal"
+DEFAULT_POINT = (256, 128, 64, 3, 4, 4)   # (TM, TN, TK, stages, producer waves, consumer waves)
+PEAK_TFLOPS = 2500.0                      # MI355X dense bf16 MFMA
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+
+
+def kernel_fingerprint() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2506_11209_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(point_key: str):
+    """HBM bytes per launch from the committed counter runs, if they were
+    taken on the current kernel sources and this launch point."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_fingerprint") != kernel_fingerprint() or t.get("point") != point_key:
+        return None
+    return t.get("traffic_bytes_per_launch")
+
+
+def cpu_baseline(wl, target_s: float = 10.0):
+    """The oracle (fp64 triple loop, as committed) on a sample of rows of C."""
+    import numpy as np
+    import oracle
+    from paper_2506_11209_amd import inputs
+    A, B = inputs.make_operands(wl.M, wl.N, wl.K, wl.dtype, wl.dist, wl.seed)
+    Ab, Bb = inputs.bits(A), inputs.bits(B)
+    lib = oracle.load()
+    t0 = time.perf_counter()
+    oracle.gemm_rows(Ab, Bb, wl.dtype, np.arange(16), lib=lib, with_abs=False)
+    t_cal = time.perf_counter() - t0
+    rows = int(max(16, min(wl.M, 16 * target_s / max(t_cal, 1e-3))))
+    rows -= rows % 16
+    t0 = time.perf_counter()
+    oracle.gemm_rows(Ab, Bb, wl.dtype, np.arange(rows), lib=lib, with_abs=False)
+    t = time.perf_counter() - t0
+    flops = 2.0 * rows * wl.N * wl.K
+    return {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": oracle.max_threads(lib),
+            "kind": "oracle",
+            "sample": "%d of %d rows of C (%dx%d by %dx%d), including operand decode; %.1f s" % (
+                rows, wl.M, wl.M, wl.K, wl.K, wl.N, t)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--point", default=None, help="TMxTNxTKxSTAGESxNPxNC")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    a = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if a.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: the GEMM has no multi-GPU path in this build "
+              "(requested --gpus %d, WORLD_SIZE %d)" % (a.gpus, world), file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2506_11209_amd import inputs
+    from paper_2506_11209_amd import wsgemm as w
+    from paper_2506_11209_amd.timing import summary, time_launches
+    from paper_2506_11209_amd.workloads import WORKLOADS
+
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    wl = WORKLOADS[WORKLOAD]
+    point = tuple(int(x) for x in a.point.split("x")) if a.point else DEFAULT_POINT
+    tm, tn, tk, stages, np_, nc = point
+    A, B = inputs.make_operands(wl.M, wl.N, wl.K, wl.dtype, wl.dist, wl.seed)
+    Ad, Bd = A.cuda(), B.cuda()
+    del A, B
+    C = torch.empty((wl.M, wl.N), dtype=torch.float32, device="cuda")
+    g = w.WsGemm(wl.M, wl.N, wl.K, (tm, tn, tk), stages, np_, nc, wl.dtype)
+    stream = torch.cuda.current_stream()
+    a_p, b_p, c_p, s_p = Ad.data_ptr(), Bd.data_ptr(), C.data_ptr(), stream.cuda_stream
+
+    def step():
+        g.run_ptrs(a_p, b_p, c_p, s_p)
+
+    dev, wall_ms = time_launches(step, a.steps, a.warmup)
+    st = g.sync_status(stream)
+    if st != w.WS_OK:
+        print("kernel reported %s" % w.ws_gemm_status_str(st), file=sys.stderr)
+        sys.exit(1)
+    sm = summary(dev)
+    value = wl.flops / (wall_ms * 1e-3) / 1e12
+    achieved = wl.flops / (sm["mean_ms"] * 1e-3) / 1e12
+    pkey = "x".join(map(str, point))
+    out = {
+        "metric": "bf16 GEMM TFLOP/s at 8192^3 (fraction of dense MFMA peak in pct_mfma_peak)",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(wall_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "pct_mfma_peak": round(100.0 * value / PEAK_TFLOPS, 2),
+        "config": {"workload": wl.name, "M": wl.M, "N": wl.N, "K": wl.K,
+                   "tile": [tm, tn, tk], "stages": stages, "producer_waves": np_,
+                   "consumer_waves": nc, "split": "%d:1" % (np_ // nc),
+                   "grid": g.info.grid, "rounds": g.info.rounds},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS, 4),
+                     "traffic": traffic_for(pkey),
+                     "kernel": "ws_gemm_kernel<%d,%d,%d,%d,%d,bf16>" % (tm, tn, tk, nc, np_ // nc),
+                     "launch_ms": {k: round(v, 5) if isinstance(v, float) else v for k, v in sm.items()}},
+    }
+    g.close()
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

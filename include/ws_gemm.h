@@ -1,0 +1,134 @@
+/*
+ * ws_gemm.h -- C ABI of the warp-specialised tiled GEMM for AMD MI355X (gfx950).
+ *
+ * Operation (paper "A Performance Model for Warp Specialization Kernels",
+ * Background, "General Matrix Multiplication"):
+ *     C = A B,   A is M x K,  B is K x N,  C is M x N,
+ * with the tiling tuple (T_M, T_N, T_K) of the same section: A is cut into
+ * T_M x T_K tiles, B into T_K x T_N tiles, C into T_M x T_N tiles.
+ *
+ * Each output tile is computed by one workgroup in which producer (DMA)
+ * wavefronts stream the A and B tiles of every K-iteration into a circular
+ * buffer in LDS and consumer (MATH) wavefronts pop them, multiply-accumulate
+ * and store the tile (Background, "The Warp Specialized GeMM Kernel in
+ * CUTLASS", and Algorithm 1).  Both arrangements of that section exist:
+ *   producer_waves == consumer_waves      one DMA warp per MATH warp, loading
+ *                                         the A tile and then the B tile;
+ *   producer_waves == 2 * consumer_waves  two DMA warps per MATH warp, one
+ *                                         loading A and one loading B.
+ * `stages` is the circular buffer's capacity in K-iterations (the buffer of
+ * Section 2.2 holding at most a fixed number of tiles).
+ *
+ * Data layout: A, B and C are dense and row-major (leading dimensions K, N
+ * and N).  A and B hold IEEE binary16 (WS_F16) or bfloat16 (WS_BF16)
+ * elements; C is always binary32.  Products are accumulated in binary32.
+ *
+ * Ownership: A, B and C are device pointers owned by the caller.  A handle
+ * owns its host-side plan and a small device word for the wait watchdog.
+ *
+ * Errors: every function returns a ws_status; nothing throws or aborts across
+ * this boundary.  Launches are asynchronous: a fault inside the kernel shows
+ * up at the caller's next synchronisation of the stream.
+ */
+#ifndef WS_GEMM_H
+#define WS_GEMM_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define WS_GEMM_ABI_VERSION 1
+
+typedef struct ws_gemm_handle* ws_gemm_t; /* opaque handle */
+
+typedef enum { WS_F16 = 0, WS_BF16 = 1 } ws_dtype;
+
+typedef enum {
+  WS_OK = 0,
+  WS_ERR_INVALID_ARG = 1,   /* NULL pointer, non-positive or oversized dimension, bad field */
+  WS_ERR_UNSUPPORTED = 2,   /* valid request with no compiled kernel or wave arrangement */
+  WS_ERR_LDS_OVERFLOW = 3,  /* stages x (A tile + B tile) does not fit in 160 KiB of LDS */
+  WS_ERR_HIP = 4,           /* a HIP runtime call failed */
+  WS_ERR_TIMEOUT = 5,       /* a producer/consumer wait exceeded its poll limit */
+  WS_ERR_NOT_DIVISIBLE = 6  /* T_M does not divide M, T_N does not divide N or T_K does not divide K */
+} ws_status;
+
+typedef struct {
+  int32_t tile_m, tile_n, tile_k; /* (T_M, T_N, T_K): powers of two, 32..256 (tile_k 32..128) */
+  int32_t producer_waves;         /* DMA wavefronts per workgroup: consumer_waves or 2x that */
+  int32_t consumer_waves;         /* MATH wavefronts per workgroup: 1 or 4 (one per SIMD) */
+  int32_t stages;                 /* circular-buffer slots, 2..8 */
+  int32_t dtype;                  /* ws_dtype of A and B */
+} ws_gemm_config;
+
+typedef struct {
+  int32_t grid;      /* persistent workgroups launched */
+  int32_t block;     /* threads per workgroup: 64 x (producer_waves + consumer_waves) */
+  int32_t lds_bytes; /* LDS per workgroup: 256 + stages x 2 x (T_M T_K + T_K T_N) */
+  int32_t tiles_m, tiles_n, tiles; /* output tiles per dimension and in total (Section 2.1) */
+  int32_t rounds;    /* dispatch rounds W = ceil(tiles / grid) (Section 2.1, "Wave") */
+  int32_t iters;     /* K-iterations per tile S = K / T_K (Section 2.1, "Stage") */
+  int32_t split;     /* 1 for one DMA warp per MATH warp, 2 for two */
+  int32_t group_m;   /* tile rows per raster group */
+  int32_t xcd_remap; /* 1 when workgroups are remapped so one XCD takes neighbouring tiles */
+} ws_gemm_plan_info;
+
+typedef struct {
+  int32_t spin_limit;     /* polls before a wait gives up (0: library default) */
+  int32_t producer_delay; /* extra ~8k-cycle sleeps per K-iteration in every producer */
+  int32_t consumer_delay; /* extra ~8k-cycle sleeps per K-iteration in every consumer */
+} ws_gemm_debug;
+
+/* ABI version of the loaded library (WS_GEMM_ABI_VERSION). */
+int32_t ws_gemm_abi_version(void);
+
+/* Static text for a status code (never NULL). */
+const char* ws_gemm_status_str(ws_status s);
+
+/* Validate a configuration and derive its launch without touching a GPU.
+ * num_cus: compute units to plan for; wgs_per_cu: resident workgroups per CU
+ * (<= 0 derives it from LDS use and wave count).  Fills *out on WS_OK. */
+ws_status ws_gemm_plan(int64_t M, int64_t N, int64_t K, const ws_gemm_config* cfg,
+                       int32_t num_cus, int32_t wgs_per_cu, ws_gemm_plan_info* out);
+
+/* Output tile (tile_m_idx, tile_n_idx) that workgroup `wg` computes in
+ * dispatch round `round` under plan `info` (as filled by ws_gemm_plan or
+ * ws_gemm_query).  Returns WS_ERR_INVALID_ARG when that workgroup has no tile
+ * in that round.  Host-only; describes the kernel's persistent tile loop. */
+ws_status ws_gemm_schedule(const ws_gemm_plan_info* info, int32_t wg, int32_t round,
+                           int32_t* tile_m_idx, int32_t* tile_n_idx);
+
+/* Validate, pick the compiled kernel for cfg, query the current device and
+ * allocate the handle.  The handle is bound to the device current at this
+ * call; later runs must use a stream of that device. */
+ws_status ws_gemm_create(int64_t M, int64_t N, int64_t K, const ws_gemm_config* cfg,
+                         ws_gemm_t* out);
+
+/* Enqueue C = A B on `stream` (0 = the null stream).  A (M x K) and B (K x N)
+ * must be 16-byte aligned device pointers, C (M x N) 4-byte aligned.  Does
+ * not synchronise.  C is fully overwritten. */
+ws_status ws_gemm_run(ws_gemm_t h, const void* A, const void* B, float* C, hipStream_t stream);
+
+/* Synchronise `stream`, then report and clear the watchdog word:
+ * WS_ERR_TIMEOUT if any wait of a previous run on this handle gave up. */
+ws_status ws_gemm_sync_status(ws_gemm_t h, hipStream_t stream);
+
+/* The plan a handle launches with. */
+ws_status ws_gemm_query(ws_gemm_t h, ws_gemm_plan_info* out);
+
+/* Test hooks: poll limit and injected producer/consumer delays for later
+ * runs (NULL restores the defaults).  Delays force the buffer-full and
+ * buffer-empty waits of Section 2.2; a tiny poll limit forces a timeout. */
+ws_status ws_gemm_set_debug(ws_gemm_t h, const ws_gemm_debug* dbg);
+
+/* Free the handle; NULL is a no-op.  Must not race with runs using it. */
+ws_status ws_gemm_destroy(ws_gemm_t h);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WS_GEMM_H */

@@ -87,10 +87,13 @@ int oracle_gemm_rows(int64_t M, int64_t N, int64_t K, const uint16_t* A, const u
   if (nrows == 0 || N == 0) return 0;
   double* Bd = (double*)malloc(sizeof(double) * (size_t)(K > 0 ? K * N : 1));
   if (!Bd) return -2;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(static)
+#endif
   for (int64_t x = 0; x < K * N; x++) Bd[x] = decode(B[x], dtype);
   int failed = 0;
 #ifdef _OPENMP
-  if (nthreads > 0) omp_set_num_threads(nthreads);
 #pragma omp parallel for schedule(dynamic, 1)
 #endif
   for (int64_t r = 0; r < nrows; r++) {

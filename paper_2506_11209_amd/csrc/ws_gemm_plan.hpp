@@ -1,0 +1,154 @@
+// Launch planning for the warp-specialised GEMM (host) and the tile raster
+// shared by host and device.
+//
+// Terms (paper, Section 2.1):
+//   output tiles  = (M / TM) * (N / TN)
+//   dispatch rounds W = ceil(tiles / workgroups)   ("waves" in the paper)
+//   K-iterations  S = K / TK                       ("stages" in the paper)
+// The paper assumes TM | M, TN | N and TK | K so that every round and every
+// K-iteration has the same cost; the planner requires the same.
+#pragma once
+
+#include <stdint.h>
+
+#if defined(__HIPCC__)
+#define WSG_HD __host__ __device__
+#else
+#define WSG_HD
+#endif
+
+namespace wsg {
+
+// Raster: schedule index v -> output tile (ti, tj).  Tiles are taken in
+// groups of group_m tile rows; inside a group, consecutive v walk down the
+// rows first, then across the columns.  A run of consecutive v therefore
+// covers a compact group_m x (run / group_m) block of output tiles.
+WSG_HD inline void tile_coords(int v, int tiles_m, int tiles_n, int group_m, int* ti, int* tj) {
+  const int per_group = group_m * tiles_n;
+  const int grp = v / per_group;
+  const int first = grp * group_m;
+  const int rows = (tiles_m - first < group_m) ? (tiles_m - first) : group_m;
+  const int rem = v - grp * per_group;
+  *ti = first + rem % rows;
+  *tj = rem / rows;
+}
+
+// Workgroup id -> schedule slot.  Workgroup g runs on XCD g % 8; the remap
+// gives XCD x the consecutive slots [x * G/8, (x+1) * G/8), so tiles that run
+// concurrently on one XCD are neighbours in the raster.  Requires G % 8 == 0.
+WSG_HD inline int xcd_slot(int g, int G) { return (g & 7) * (G >> 3) + (g >> 3); }
+
+struct PlanIn {
+  int64_t M, N, K;
+  int32_t tile_m, tile_n, tile_k;
+  int32_t producer_waves, consumer_waves, stages, dtype;
+  int32_t num_cus;     // compute units on the device
+  int32_t wgs_per_cu;  // resident workgroups per CU (<= 0: derive from LDS and waves)
+};
+
+struct PlanOut {
+  int32_t grid, block, lds_bytes;
+  int32_t tiles_m, tiles_n, tiles, rounds, iters;
+  int32_t split, group_m, xcd_remap;
+};
+
+enum PlanStatus {
+  kPlanOk = 0,
+  kPlanInvalid = 1,
+  kPlanNotDivisible = 6,
+  kPlanUnsupported = 2,
+  kPlanLdsOverflow = 3,
+};
+
+constexpr int kLdsLimit = 163840;   // bytes of LDS per workgroup on gfx950
+constexpr int kPlanHeaderBytes = 256;
+constexpr int kPlanMaxStages = 8;
+constexpr int kMaxWavesPerCu = 32;
+
+inline bool is_pow2_in(int x, int lo, int hi) {
+  return x >= lo && x <= hi && (x & (x - 1)) == 0;
+}
+
+// Pure host computation: validates a configuration and derives the launch.
+inline int plan_launch(const PlanIn& in, PlanOut* out) {
+  if (!out) return kPlanInvalid;
+  *out = PlanOut{};
+  if (in.M <= 0 || in.N <= 0 || in.K <= 0) return kPlanInvalid;
+  if (in.M > (1 << 30) || in.N > (1 << 30) || in.K > (1 << 30)) return kPlanInvalid;
+  if (in.dtype != 0 && in.dtype != 1) return kPlanInvalid;
+  if (!is_pow2_in(in.tile_m, 32, 256) || !is_pow2_in(in.tile_n, 32, 256) ||
+      !is_pow2_in(in.tile_k, 32, 128))
+    return kPlanInvalid;
+  const int nc = in.consumer_waves, np = in.producer_waves;
+  if (nc != 1 && nc != 4) return kPlanUnsupported;
+  if (np != nc && np != 2 * nc) return kPlanUnsupported;
+  const int wm = in.tile_m / (nc == 4 ? 2 : 1), wn = in.tile_n / (nc == 4 ? 2 : 1);
+  if (wm < 32 || wn < 32 || wm * wn > 128 * 64) return kPlanUnsupported;
+  if (in.stages < 2 || in.stages > kPlanMaxStages) return kPlanInvalid;
+  if (in.M % in.tile_m || in.N % in.tile_n || in.K % in.tile_k) return kPlanNotDivisible;
+  // element offsets inside one tile panel are 32-bit
+  // byte offsets inside one tile panel (A, B and the C epilogue) are 32-bit
+  if ((int64_t)in.tile_m * in.K * 2 >= (1ll << 31) || (int64_t)in.tile_k * in.N * 2 >= (1ll << 31) ||
+      (int64_t)in.tile_m * in.N * 4 >= (1ll << 31))
+    return kPlanInvalid;
+  const int64_t stage = 2ll * (in.tile_m * in.tile_k + in.tile_k * in.tile_n);
+  const int64_t lds = kPlanHeaderBytes + in.stages * stage;
+  if (lds > kLdsLimit) return kPlanLdsOverflow;
+  if (in.num_cus <= 0) return kPlanInvalid;
+
+  const int64_t tm = in.M / in.tile_m, tn = in.N / in.tile_n;
+  if (tm * tn >= (1ll << 31)) return kPlanInvalid;
+  const int tiles = (int)(tm * tn);
+  const int waves = nc + np;
+  int occ = in.wgs_per_cu;
+  if (occ <= 0) {
+    occ = (int)(kLdsLimit / lds);
+    if (kMaxWavesPerCu / waves < occ) occ = kMaxWavesPerCu / waves;
+  }
+  if (occ < 1) occ = 1;
+  int64_t slots = (int64_t)in.num_cus * occ;
+  const int grid = (int)(tiles < slots ? tiles : slots);
+  const int xcd_remap = (grid % 8 == 0) ? 1 : 0;  // the remap needs whole XCD groups
+
+  // group_m: choose the tile-row group that minimises the A + B panel width a
+  // single XCD touches per round.
+  const int per_xcd = xcd_remap ? grid / 8 : grid;
+  int best_gm = 1;
+  int64_t best_cost = -1;
+  for (int gm = 1; gm <= tm; gm *= 2) {
+    const int64_t rows = gm;
+    int64_t cols = (per_xcd + rows - 1) / rows;
+    if (cols > tn) cols = tn;
+    const int64_t cost = rows * in.tile_m + cols * in.tile_n;
+    if (best_cost < 0 || cost < best_cost) {
+      best_cost = cost;
+      best_gm = gm;
+    }
+  }
+
+  out->grid = grid;
+  out->block = 64 * waves;
+  out->lds_bytes = (int32_t)lds;
+  out->tiles_m = (int32_t)tm;
+  out->tiles_n = (int32_t)tn;
+  out->tiles = tiles;
+  out->rounds = (tiles + grid - 1) / grid;
+  out->iters = (int32_t)(in.K / in.tile_k);
+  out->split = np / nc;
+  out->group_m = best_gm;
+  out->xcd_remap = xcd_remap;
+  return kPlanOk;
+}
+
+// Output tile computed by workgroup g in dispatch round r of a plan
+// (returns false when that workgroup has no tile in that round).
+inline bool scheduled_tile(const PlanOut& p, int g, int r, int* ti, int* tj) {
+  if (g < 0 || g >= p.grid || r < 0) return false;
+  const int slot = p.xcd_remap ? xcd_slot(g, p.grid) : g;
+  const int64_t v = (int64_t)r * p.grid + slot;
+  if (v >= p.tiles) return false;
+  tile_coords((int)v, p.tiles_m, p.tiles_n, p.group_m, ti, tj);
+  return true;
+}
+
+}  // namespace wsg

@@ -1,0 +1,211 @@
+"""ctypes binding of libwsgemm.so (declared in include/ws_gemm.h).
+
+Functions carry the C names and only marshal arguments; every step of the
+GEMM runs in the library's HIP kernels.  Importing this module raises if the
+library has not been built (``python -m paper_2506_11209_amd.build``): there
+is no fallback path.
+
+``WsGemm`` is a convenience wrapper over torch device tensors and streams.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIBRARY = os.path.join(_HERE, "libwsgemm.so")
+
+if not os.path.exists(LIBRARY):
+    raise ImportError("%s is not built; run `python -m paper_2506_11209_amd.build`" % LIBRARY)
+
+_lib = ctypes.CDLL(LIBRARY)
+
+WS_F16, WS_BF16 = 0, 1
+DTYPE_CODES = {"f16": WS_F16, "bf16": WS_BF16}
+
+WS_OK = 0
+WS_ERR_INVALID_ARG = 1
+WS_ERR_UNSUPPORTED = 2
+WS_ERR_LDS_OVERFLOW = 3
+WS_ERR_HIP = 4
+WS_ERR_TIMEOUT = 5
+WS_ERR_NOT_DIVISIBLE = 6
+
+
+class ws_gemm_config(ctypes.Structure):
+    _fields_ = [("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32), ("tile_k", ctypes.c_int32),
+                ("producer_waves", ctypes.c_int32), ("consumer_waves", ctypes.c_int32),
+                ("stages", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class ws_gemm_plan_info(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "grid", "block", "lds_bytes", "tiles_m", "tiles_n", "tiles", "rounds", "iters", "split",
+        "group_m", "xcd_remap")]
+
+    def as_dict(self) -> dict:
+        return {n: getattr(self, n) for n, _ in self._fields_}
+
+
+class ws_gemm_debug(ctypes.Structure):
+    _fields_ = [("spin_limit", ctypes.c_int32), ("producer_delay", ctypes.c_int32),
+                ("consumer_delay", ctypes.c_int32)]
+
+
+_h = ctypes.c_void_p
+_p = ctypes.c_void_p
+_i64, _i32 = ctypes.c_int64, ctypes.c_int32
+
+_lib.ws_gemm_abi_version.argtypes = []
+_lib.ws_gemm_abi_version.restype = _i32
+_lib.ws_gemm_status_str.argtypes = [_i32]
+_lib.ws_gemm_status_str.restype = ctypes.c_char_p
+_lib.ws_gemm_plan.argtypes = [_i64, _i64, _i64, ctypes.POINTER(ws_gemm_config), _i32, _i32,
+                              ctypes.POINTER(ws_gemm_plan_info)]
+_lib.ws_gemm_plan.restype = _i32
+_lib.ws_gemm_schedule.argtypes = [ctypes.POINTER(ws_gemm_plan_info), _i32, _i32,
+                                  ctypes.POINTER(_i32), ctypes.POINTER(_i32)]
+_lib.ws_gemm_schedule.restype = _i32
+_lib.ws_gemm_create.argtypes = [_i64, _i64, _i64, ctypes.POINTER(ws_gemm_config),
+                                ctypes.POINTER(_h)]
+_lib.ws_gemm_create.restype = _i32
+_lib.ws_gemm_run.argtypes = [_h, _p, _p, _p, _p]
+_lib.ws_gemm_run.restype = _i32
+_lib.ws_gemm_sync_status.argtypes = [_h, _p]
+_lib.ws_gemm_sync_status.restype = _i32
+_lib.ws_gemm_query.argtypes = [_h, ctypes.POINTER(ws_gemm_plan_info)]
+_lib.ws_gemm_query.restype = _i32
+_lib.ws_gemm_set_debug.argtypes = [_h, ctypes.POINTER(ws_gemm_debug)]
+_lib.ws_gemm_set_debug.restype = _i32
+_lib.ws_gemm_destroy.argtypes = [_h]
+_lib.ws_gemm_destroy.restype = _i32
+
+
+def library() -> ctypes.CDLL:
+    return _lib
+
+
+def config(tile=(128, 128, 32), stages=3, producer_waves=4, consumer_waves=4, dtype="bf16"):
+    tm, tn, tk = tile
+    return ws_gemm_config(tm, tn, tk, producer_waves, consumer_waves, stages, DTYPE_CODES[dtype])
+
+
+# -- C names -----------------------------------------------------------------
+
+def ws_gemm_abi_version() -> int:
+    return _lib.ws_gemm_abi_version()
+
+
+def ws_gemm_status_str(status: int) -> str:
+    return _lib.ws_gemm_status_str(status).decode()
+
+
+def ws_gemm_plan(M, N, K, cfg: ws_gemm_config, num_cus: int, wgs_per_cu: int = 0):
+    info = ws_gemm_plan_info()
+    s = _lib.ws_gemm_plan(M, N, K, ctypes.byref(cfg), num_cus, wgs_per_cu, ctypes.byref(info))
+    return s, info
+
+
+def ws_gemm_schedule(info: ws_gemm_plan_info, wg: int, rnd: int):
+    ti, tj = _i32(-1), _i32(-1)
+    s = _lib.ws_gemm_schedule(ctypes.byref(info), wg, rnd, ctypes.byref(ti), ctypes.byref(tj))
+    return s, ti.value, tj.value
+
+
+def ws_gemm_create(M, N, K, cfg: ws_gemm_config):
+    h = _h()
+    s = _lib.ws_gemm_create(M, N, K, ctypes.byref(cfg), ctypes.byref(h))
+    return s, h
+
+
+def ws_gemm_run(h, A_ptr: int, B_ptr: int, C_ptr: int, stream_ptr: int = 0) -> int:
+    return _lib.ws_gemm_run(h, _p(A_ptr), _p(B_ptr), _p(C_ptr), _p(stream_ptr))
+
+
+def ws_gemm_sync_status(h, stream_ptr: int = 0) -> int:
+    return _lib.ws_gemm_sync_status(h, _p(stream_ptr))
+
+
+def ws_gemm_query(h):
+    info = ws_gemm_plan_info()
+    s = _lib.ws_gemm_query(h, ctypes.byref(info))
+    return s, info
+
+
+def ws_gemm_set_debug(h, dbg: ws_gemm_debug | None) -> int:
+    return _lib.ws_gemm_set_debug(h, ctypes.byref(dbg) if dbg is not None else None)
+
+
+def ws_gemm_destroy(h) -> int:
+    return _lib.ws_gemm_destroy(h)
+
+
+# -- convenience over torch ----------------------------------------------------
+
+class WsGemmError(RuntimeError):
+    def __init__(self, where: str, status: int):
+        super().__init__("%s: %s (status %d)" % (where, ws_gemm_status_str(status), status))
+        self.status = status
+
+
+class WsGemm:
+    """A created plan for one (M, N, K, configuration); call it on torch tensors."""
+
+    def __init__(self, M, N, K, tile=(128, 128, 32), stages=3, producer_waves=4,
+                 consumer_waves=4, dtype="bf16"):
+        self.M, self.N, self.K = M, N, K
+        self.dtype = dtype
+        self.cfg = config(tile, stages, producer_waves, consumer_waves, dtype)
+        s, self._h = ws_gemm_create(M, N, K, self.cfg)
+        if s != WS_OK:
+            self._h = None
+            raise WsGemmError("ws_gemm_create", s)
+        s, self.info = ws_gemm_query(self._h)
+        if s != WS_OK:
+            raise WsGemmError("ws_gemm_query", s)
+
+    def _check(self, t, shape, dtype_name):
+        import torch
+        want = {"f16": torch.float16, "bf16": torch.bfloat16, "f32": torch.float32}[dtype_name]
+        if t.device.type != "cuda" or t.dtype != want or tuple(t.shape) != shape or not t.is_contiguous():
+            raise ValueError("expected a contiguous %s cuda tensor of shape %s, got %s %s %s" % (
+                dtype_name, shape, t.dtype, tuple(t.shape), t.device))
+
+    def __call__(self, A, B, C=None, stream=None):
+        import torch
+        self._check(A, (self.M, self.K), self.dtype)
+        self._check(B, (self.K, self.N), self.dtype)
+        if C is None:
+            C = torch.empty((self.M, self.N), dtype=torch.float32, device=A.device)
+        self._check(C, (self.M, self.N), "f32")
+        st = stream if stream is not None else torch.cuda.current_stream(A.device)
+        s = ws_gemm_run(self._h, A.data_ptr(), B.data_ptr(), C.data_ptr(), st.cuda_stream)
+        if s != WS_OK:
+            raise WsGemmError("ws_gemm_run", s)
+        return C
+
+    def run_ptrs(self, A_ptr, B_ptr, C_ptr, stream_ptr=0):
+        s = ws_gemm_run(self._h, A_ptr, B_ptr, C_ptr, stream_ptr)
+        if s != WS_OK:
+            raise WsGemmError("ws_gemm_run", s)
+
+    def sync_status(self, stream=None) -> int:
+        import torch
+        st = stream if stream is not None else torch.cuda.current_stream()
+        return ws_gemm_sync_status(self._h, st.cuda_stream)
+
+    def set_debug(self, spin_limit=0, producer_delay=0, consumer_delay=0):
+        s = ws_gemm_set_debug(self._h, ws_gemm_debug(spin_limit, producer_delay, consumer_delay))
+        if s != WS_OK:
+            raise WsGemmError("ws_gemm_set_debug", s)
+
+    def close(self):
+        if self._h is not None:
+            ws_gemm_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

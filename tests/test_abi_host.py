@@ -1,0 +1,167 @@
+"""C-ABI host logic: symbols, validation, planning and the tile schedule (no GPU)."""
+import os
+import re
+
+import pytest
+
+from paper_2506_11209_amd import wsgemm as w
+from paper_2506_11209_amd.workloads import WORKLOADS
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+GOLDEN = os.path.join(ROOT, "tests", "golden")
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "ws_gemm.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ws_gemm_\w+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 9
+    lib = w.library()
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_abi_version_and_status_text():
+    assert w.ws_gemm_abi_version() == 1
+    for s in range(7):
+        assert w.ws_gemm_status_str(s) and w.ws_gemm_status_str(s) != "unknown status"
+    assert w.ws_gemm_status_str(99) == "unknown status"
+
+
+def cfg(tile=(256, 128, 64), stages=3, np_=4, nc=4, dtype="bf16"):
+    return w.config(tile, stages, np_, nc, dtype)
+
+
+def test_plan_headline_shape():
+    s, info = w.ws_gemm_plan(8192, 8192, 8192, cfg(), 256, 1)
+    assert s == w.WS_OK
+    d = info.as_dict()
+    assert d["tiles"] == 32 * 64 and d["grid"] == 256 and d["rounds"] == 8 and d["iters"] == 128
+    assert d["block"] == 512 and d["split"] == 1 and d["xcd_remap"] == 1
+    assert d["lds_bytes"] == 256 + 3 * 2 * (256 * 64 + 64 * 128)
+
+
+@pytest.mark.parametrize("name", sorted(WORKLOADS))
+def test_plan_every_workload_point(name):
+    wl = WORKLOADS[name]
+    for (tm, tn, tk, stages, np_, nc) in wl.points:
+        s, info = w.ws_gemm_plan(wl.M, wl.N, wl.K, cfg((tm, tn, tk), stages, np_, nc, wl.dtype), 256, 1)
+        stage = 2 * (tm * tk + tk * tn)
+        if 256 + stages * stage > 163840:
+            assert s == w.WS_ERR_LDS_OVERFLOW
+            continue
+        assert s == w.WS_OK, (name, tm, tn, tk, stages, np_, nc, w.ws_gemm_status_str(s))
+        tiles = (wl.M // tm) * (wl.N // tn)
+        assert info.tiles == tiles and info.iters == wl.K // tk
+        assert info.grid == min(tiles, 256)
+        assert info.rounds == -(-tiles // info.grid)
+        assert info.split == np_ // nc and info.block == 64 * (np_ + nc)
+
+
+def test_lds_overflow_case_from_the_sweep():
+    # (256,128,64) x 4 stages = 192 KiB + header > 160 KiB
+    s, _ = w.ws_gemm_plan(8192, 8192, 8192, cfg((256, 128, 64), 4), 256, 1)
+    assert s == w.WS_ERR_LDS_OVERFLOW
+
+
+@pytest.mark.parametrize("M,N,K,tile,status", [
+    (8192, 8192, 8192 + 32, (256, 128, 64), w.WS_ERR_NOT_DIVISIBLE),
+    (8192 + 64, 8192, 8192, (256, 128, 64), w.WS_ERR_NOT_DIVISIBLE),
+    (8192, 8192 + 32, 8192, (256, 128, 64), w.WS_ERR_NOT_DIVISIBLE),
+    (0, 8192, 8192, (256, 128, 64), w.WS_ERR_INVALID_ARG),
+    (8192, -1, 8192, (256, 128, 64), w.WS_ERR_INVALID_ARG),
+    (8192, 8192, 8192, (48, 128, 64), w.WS_ERR_INVALID_ARG),
+    (8192, 8192, 8192, (512, 128, 64), w.WS_ERR_INVALID_ARG),
+    (8192, 8192, 8192, (256, 128, 16), w.WS_ERR_INVALID_ARG),
+    (8192, 8192, 8192, (256, 256, 32), w.WS_ERR_UNSUPPORTED),  # 128x128 wave tile
+])
+def test_plan_rejections(M, N, K, tile, status):
+    s, _ = w.ws_gemm_plan(M, N, K, cfg(tile), 256, 1)
+    assert s == status, w.ws_gemm_status_str(s)
+
+
+@pytest.mark.parametrize("np_,nc,stages,status", [
+    (3, 4, 3, w.WS_ERR_UNSUPPORTED), (4, 2, 3, w.WS_ERR_UNSUPPORTED), (4, 4, 1, w.WS_ERR_INVALID_ARG),
+    (4, 4, 9, w.WS_ERR_INVALID_ARG), (16, 4, 2, w.WS_ERR_UNSUPPORTED),
+])
+def test_plan_rejects_wave_and_stage_counts(np_, nc, stages, status):
+    s, _ = w.ws_gemm_plan(4096, 4096, 4096, cfg((128, 128, 32), stages, np_, nc), 256, 1)
+    assert s == status
+
+
+def test_plan_bad_dtype_and_cus():
+    c = cfg()
+    c.dtype = 7
+    assert w.ws_gemm_plan(8192, 8192, 8192, c, 256, 1)[0] == w.WS_ERR_INVALID_ARG
+    assert w.ws_gemm_plan(8192, 8192, 8192, cfg(), 0, 1)[0] == w.WS_ERR_INVALID_ARG
+
+
+def test_null_handles_are_rejected():
+    assert w.ws_gemm_destroy(None) == w.WS_OK
+    assert w.ws_gemm_run(None, 16, 16, 16, 0) == w.WS_ERR_INVALID_ARG
+    assert w.ws_gemm_sync_status(None, 0) == w.WS_ERR_INVALID_ARG
+    assert w.ws_gemm_query(None)[0] == w.WS_ERR_INVALID_ARG
+    assert w.ws_gemm_set_debug(None, None) == w.WS_ERR_INVALID_ARG
+
+
+def _schedule(info):
+    seen = {}
+    for r in range(info.rounds + 1):
+        for g in range(info.grid):
+            s, ti, tj = w.ws_gemm_schedule(info, g, r)
+            if s == w.WS_OK:
+                assert (ti, tj) not in seen, "tile computed twice"
+                seen[(ti, tj)] = (g, r)
+            else:
+                assert r * info.grid + g >= info.tiles or r == info.rounds
+    return seen
+
+
+@pytest.mark.parametrize("shape,tile,cus", [
+    ((8192, 8192), (256, 128, 64), 256), ((4096, 4096), (128, 128, 32), 256),
+    ((16384, 256), (128, 64, 64), 256), ((2048, 2048), (128, 128, 64), 256),
+    ((1024, 3072), (64, 64, 32), 84), ((640, 448), (64, 64, 32), 100),
+])
+def test_schedule_covers_every_tile_once(shape, tile, cus):
+    M, N = shape
+    s, info = w.ws_gemm_plan(M, N, 1024, cfg(tile, 2), cus, 1)
+    assert s == w.WS_OK
+    seen = _schedule(info)
+    assert len(seen) == info.tiles
+    assert {k for k in seen} == {(i, j) for i in range(info.tiles_m) for j in range(info.tiles_n)}
+
+
+def test_xcd_blocks_are_compact():
+    """Tiles running together on one XCD form a group_m x (32/group_m) block."""
+    s, info = w.ws_gemm_plan(8192, 8192, 8192, cfg(), 256, 1)
+    for r in range(info.rounds):
+        for x in range(8):
+            tiles = [w.ws_gemm_schedule(info, g, r)[1:] for g in range(x, 256, 8)]
+            rows = {t[0] for t in tiles}
+            cols = {t[1] for t in tiles}
+            assert len(rows) * len(cols) == 32 and len(rows) == info.group_m
+
+
+def test_paper_wave_example():
+    """Section 2.1: 256 output tiles on 84 SMs take four waves; 80 SMs get
+    three tiles and four SMs get four (tests/golden/paper_wave_example.txt)."""
+    vals = {}
+    for line in open(os.path.join(GOLDEN, "paper_wave_example.txt")):
+        line = line.split("#")[0].strip()
+        if line:
+            k, v = line.split("=")
+            vals[k.strip()] = int(v)
+    # 256 tiles of 64x64 on a 1024x1024 output, one workgroup per SM
+    s, info = w.ws_gemm_plan(1024, 1024, 256, cfg((64, 64, 32), 2, 1, 1), vals["sms"], 1)
+    assert s == w.WS_OK and info.tiles == vals["tiles"] and info.grid == vals["sms"]
+    assert info.rounds == vals["waves"]
+    seen = _schedule(info)
+    per_wg = {}
+    for (g, r) in seen.values():
+        per_wg[g] = per_wg.get(g, 0) + 1
+    counts = sorted(per_wg.values())
+    assert counts.count(3) == vals["sms_with_3"] and counts.count(4) == vals["sms_with_4"]

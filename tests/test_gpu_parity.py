@@ -1,0 +1,216 @@
+"""Parity of the HIP kernels (through the C ABI) with the CPU oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2506_11209_amd import inputs
+from paper_2506_11209_amd.workloads import WORKLOADS
+from tests.gpu_helpers import (check_full, check_rows, freivalds, log, run_gpu, sample_rows)
+
+pytestmark = pytest.mark.gpu
+
+LDS_LIMIT = 163840
+
+
+def fits(tile, stages):
+    tm, tn, tk = tile
+    return 256 + stages * 2 * (tm * tk + tk * tn) <= LDS_LIMIT
+
+
+# ---------------------------------------------------------------------------
+# The 256^3 fp16 small-integer workload: bit-exact.
+# ---------------------------------------------------------------------------
+def test_int256_f16_bit_exact():
+    wl = WORKLOADS["gemm_256x256x256_f16_int4"]
+    A, B = inputs.make_operands(wl.M, wl.N, wl.K, wl.dtype, wl.dist, wl.seed)
+    (tm, tn, tk, stages, np_, nc), = wl.points
+    log("case int256 f16 tile=%s stages=%d np=%d nc=%d" % ((tm, tn, tk), stages, np_, nc))
+    C = run_gpu(A, B, (tm, tn, tk), stages, np_, nc, wl.dtype)
+    r = check_full(C, A, B, wl.dtype, exact=True)
+    assert r["ok"], r
+
+
+# ---------------------------------------------------------------------------
+# Every compiled kernel family on small-integer operands: any indexing,
+# swizzle, slot or role mistake changes an exact integer result.
+# Shapes span several tiles in M and N, a ragged last round and S > stages.
+# ---------------------------------------------------------------------------
+FAMILIES = []
+for dt in ("bf16", "f16"):
+    for split in (1, 2):
+        for tk in (32, 64):
+            for (tm, tn) in ((32, 32), (64, 64)):
+                FAMILIES.append(((tm, tn, tk), 1, split, dt))
+            for (tm, tn) in ((64, 64), (64, 128), (128, 64), (128, 128), (128, 256), (256, 128)):
+                FAMILIES.append(((tm, tn, tk), 4, split, dt))
+
+
+@pytest.mark.parametrize("tile,nc,split,dtype", FAMILIES,
+                         ids=lambda x: "x".join(map(str, x)) if isinstance(x, tuple) else str(x))
+def test_family_exact_on_integers(tile, nc, split, dtype):
+    tm, tn, tk = tile
+    M, N, K = 3 * tm, 5 * tn, 7 * tk  # 15 tiles, S = 7
+    stages = 2 if fits(tile, 3) is False else 3
+    A, B = inputs.make_operands(M, N, K, dtype, "int4", 100 + tm + tn + tk)
+    log("case family tile=%s nc=%d split=%d %s" % (tile, nc, split, dtype))
+    C = run_gpu(A, B, tile, stages, nc * split, nc, dtype)
+    r = check_full(C, A, B, dtype, exact=True)
+    assert r["ok"], r
+
+
+@pytest.mark.parametrize("stages", [2, 3, 4])
+@pytest.mark.parametrize("K", [64, 128, 192, 256])  # S = 1, 2, 3, 4 around the ring depth
+def test_ring_depth_edges(stages, K):
+    tile = (128, 128, 64)
+    A, B = inputs.make_operands(256, 512, K, "bf16", "int4", 7 + K)
+    log("case ring stages=%d K=%d" % (stages, K))
+    C = run_gpu(A, B, tile, stages, 4, 4, "bf16")
+    assert check_full(C, A, B, "bf16", exact=True)["ok"]
+
+
+def test_single_tile_single_iteration():
+    A, B = inputs.make_operands(64, 64, 32, "f16", "int4", 3)
+    C = run_gpu(A, B, (64, 64, 32), 2, 1, 1, "f16")
+    assert check_full(C, A, B, "f16", exact=True)["ok"]
+
+
+def test_multi_round_exact():
+    """512 output tiles on a 256-workgroup grid: two dispatch rounds."""
+    A, B = inputs.make_operands(4096, 4096, 128, "bf16", "int4", 11)
+    log("case multi-round 4096x4096x128")
+    C = run_gpu(A, B, (256, 128, 64), 3, 4, 4, "bf16")
+    assert check_full(C, A, B, "bf16", exact=True)["ok"]
+
+
+@pytest.mark.parametrize("tile,stages,np_,nc,dtype", [
+    ((256, 128, 64), 3, 4, 4, "bf16"), ((128, 256, 32), 4, 8, 4, "bf16"),
+    ((128, 128, 32), 3, 4, 4, "f16"), ((64, 64, 64), 2, 2, 1, "bf16"),
+])
+def test_random_within_tolerance(tile, stages, np_, nc, dtype):
+    A, B = inputs.make_operands(768, 1024, 1536, dtype, "normal", 21)
+    log("case random tile=%s" % (tile,))
+    C = run_gpu(A, B, tile, stages, np_, nc, dtype)
+    r = check_full(C, A, B, dtype, exact=False)
+    assert r["ok"], r
+
+
+def test_output_overwritten_and_deterministic():
+    A, B = inputs.make_operands(512, 512, 1024, "bf16", "normal", 5)
+    C1 = run_gpu(A, B, (128, 128, 64), 3, 4, 4, "bf16", C_fill=float("nan"), repeats=1)
+    C2 = run_gpu(A, B, (128, 128, 64), 3, 4, 4, "bf16", C_fill=123.0, repeats=3)
+    assert np.all(np.isfinite(C1))
+    assert np.array_equal(C1.view(np.uint32), C2.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# Protocol stress: injected delays force buffer-full and buffer-empty waits
+# (the paper's fast / slow DMA scenarios); a tiny poll limit forces the
+# watchdog, and every wave still exits.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("pdelay,cdelay", [(3, 0), (0, 3)])
+def test_delays_keep_results_exact(pdelay, cdelay):
+    from paper_2506_11209_amd import wsgemm as w
+    A, B = inputs.make_operands(512, 512, 1024, "bf16", "int4", 9)
+    log("case delays p=%d c=%d" % (pdelay, cdelay))
+    g = w.WsGemm(512, 512, 1024, (128, 128, 64), 2, 4, 4, "bf16")
+    try:
+        g.set_debug(0, pdelay, cdelay)
+        C = g(A.cuda(), B.cuda())
+        assert g.sync_status() == w.WS_OK
+        assert check_full(C.cpu().numpy(), A, B, "bf16", exact=True)["ok"]
+    finally:
+        g.close()
+
+
+def test_watchdog_reports_timeout_then_recovers():
+    from paper_2506_11209_amd import wsgemm as w
+    A, B = inputs.make_operands(512, 512, 1024, "bf16", "int4", 10)
+    log("case watchdog")
+    g = w.WsGemm(512, 512, 1024, (128, 128, 64), 2, 4, 4, "bf16")
+    try:
+        Ad, Bd = A.cuda(), B.cuda()
+        g.set_debug(1, 20, 0)  # one poll allowed, producers ~160k cycles late
+        g(Ad, Bd)
+        assert g.sync_status() == w.WS_ERR_TIMEOUT
+        assert g.sync_status() == w.WS_OK  # cleared
+        g.set_debug(0, 0, 0)
+        C = g(Ad, Bd)
+        assert g.sync_status() == w.WS_OK
+        assert check_full(C.cpu().numpy(), A, B, "bf16", exact=True)["ok"]
+    finally:
+        g.close()
+
+
+def test_run_rejects_misaligned_pointers():
+    from paper_2506_11209_amd import wsgemm as w
+    g = w.WsGemm(256, 256, 256, (64, 64, 32), 2, 1, 1, "f16")
+    try:
+        buf = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
+        p = buf.data_ptr()
+        assert w.ws_gemm_run(g._h, p + 2, p, p, 0) == w.WS_ERR_INVALID_ARG
+        assert w.ws_gemm_run(g._h, p, p + 8, p, 0) == w.WS_ERR_INVALID_ARG
+        assert w.ws_gemm_run(g._h, p, p, p + 2, 0) == w.WS_ERR_INVALID_ARG
+    finally:
+        g.close()
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads, in the launch configurations the benchmark and the
+# sweep time: sampled oracle rows plus Freivalds' check over all of C.
+# ---------------------------------------------------------------------------
+class _Full:
+    def __init__(self, name):
+        wl = WORKLOADS[name]
+        self.wl = wl
+        self.A, self.B = inputs.make_operands(wl.M, wl.N, wl.K, wl.dtype, wl.dist, wl.seed)
+        self.Ab, self.Bb = inputs.bits(self.A), inputs.bits(self.B)
+        self.Ad, self.Bd = self.A.cuda(), self.B.cuda()
+        self.rows = sample_rows(wl.M, 256)
+        self.ref = oracle.gemm_rows(self.Ab, self.Bb, wl.dtype, self.rows)
+        self.A64 = self.A.double().numpy()
+        self.B64 = self.B.double().numpy()
+        self.absA, self.absB = np.abs(self.A64), np.abs(self.B64)
+
+
+_cache = {}
+
+
+def full(name):
+    if name not in _cache:
+        _cache.clear()
+        _cache[name] = _Full(name)
+    return _cache[name]
+
+
+FULL_CASES = [(name, pt) for name in ("gemm_4096x4096x4096_bf16_normal",
+                                      "gemm_8192x8192x8192_bf16_normal",
+                                      "gemm_16384x256x8192_bf16_uniform",
+                                      "gemm_2048x2048x32768_bf16_normal_k")
+              for pt in WORKLOADS[name].points]
+
+
+@pytest.mark.parametrize("name,point", FULL_CASES, ids=lambda x: "x".join(map(str, x)) if isinstance(x, tuple) else x)
+def test_full_size_workload(name, point):
+    from paper_2506_11209_amd import wsgemm as w
+    tm, tn, tk, stages, np_, nc = point
+    f = full(name)
+    wl = f.wl
+    log("case full %s point=%s" % (name, point))
+    if not fits((tm, tn, tk), stages):
+        s, _ = w.ws_gemm_create(wl.M, wl.N, wl.K, w.config((tm, tn, tk), stages, np_, nc, wl.dtype))
+        assert s == w.WS_ERR_LDS_OVERFLOW
+        return
+    g = w.WsGemm(wl.M, wl.N, wl.K, (tm, tn, tk), stages, np_, nc, wl.dtype)
+    try:
+        C = torch.full((wl.M, wl.N), float("nan"), dtype=torch.float32, device="cuda")
+        g(f.Ad, f.Bd, C)
+        g(f.Ad, f.Bd, C)
+        assert g.sync_status() == w.WS_OK
+        Ch = C.cpu().numpy()
+    finally:
+        g.close()
+    r = check_rows(Ch, f.Ab, f.Bb, wl.dtype, f.rows, ref=f.ref)
+    assert r["ok"], r
+    ok, worst = freivalds(Ch, f.A64, f.B64, f.absA, f.absB)
+    assert ok, worst
