@@ -88,6 +88,10 @@ int32_t ws_gemm_abi_version(void);
 /* Static text for a status code (never NULL). */
 const char* ws_gemm_status_str(ws_status s);
 
+/* The HIP call and error text behind the last WS_ERR_HIP returned on this
+ * thread ("" if none).  Static per-thread storage; never NULL. */
+const char* ws_gemm_last_error(void);
+
 /* Validate a configuration and derive its launch without touching a GPU.
  * num_cus: compute units to plan for; wgs_per_cu: resident workgroups per CU
  * (<= 0 derives it from LDS use and wave count).  Fills *out on WS_OK. */

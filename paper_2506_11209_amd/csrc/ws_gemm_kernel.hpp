@@ -77,12 +77,26 @@ struct KernelArgs {
   int32_t* err;            // set to 1 when a bounded wait gives up
 };
 
+// XOR swizzle of the 16-byte chunks of A-tile row r.  It depends on r & 31
+// only, so rows 32 apart share it and the consumer can fold whole 32-row
+// blocks into instruction offsets.  Rows 0..15 read by one ds_read_b128 fall
+// on distinct 16-byte bank groups (for both 128- and 256-byte bank rows).
 template <int TK>
-__device__ __forceinline__ int swz_a(int r) {
+__host__ __device__ constexpr int swz_a(int r) {
   if constexpr (TK == 32) return ((r >> 1) ^ (r >> 3)) & 3;
-  else if constexpr (TK == 64) return (r ^ (r >> 3)) & 7;
+  else if constexpr (TK == 64) return (r ^ ((r >> 3) & 1)) & 7;
   else return r & 15;
 }
+
+template <int TK>
+constexpr bool swz_a_period32() {
+  for (int r = 0; r < 256; ++r)
+    if (swz_a<TK>(r) != swz_a<TK>(r & 31) || swz_a<TK>(r) < 0 || swz_a<TK>(r) >= TK / 8)
+      return false;
+  return true;
+}
+static_assert(swz_a_period32<32>() && swz_a_period32<64>() && swz_a_period32<128>(),
+              "A swizzle must repeat every 32 rows and stay inside the row");
 
 __device__ __forceinline__ uint32_t lds_peek(WSG_LDS uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);

@@ -12,6 +12,11 @@ from __future__ import annotations
 import ctypes
 import os
 
+# torch ships its own HIP runtime.  It must be the one loaded first: the
+# library's libamdhip64 dependency then resolves to that same copy, and the
+# process holds a single runtime (two copies do not share the device).
+import torch  # noqa: F401
+
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIBRARY = os.path.join(_HERE, "libwsgemm.so")
 
@@ -60,6 +65,8 @@ _lib.ws_gemm_abi_version.argtypes = []
 _lib.ws_gemm_abi_version.restype = _i32
 _lib.ws_gemm_status_str.argtypes = [_i32]
 _lib.ws_gemm_status_str.restype = ctypes.c_char_p
+_lib.ws_gemm_last_error.argtypes = []
+_lib.ws_gemm_last_error.restype = ctypes.c_char_p
 _lib.ws_gemm_plan.argtypes = [_i64, _i64, _i64, ctypes.POINTER(ws_gemm_config), _i32, _i32,
                               ctypes.POINTER(ws_gemm_plan_info)]
 _lib.ws_gemm_plan.restype = _i32
@@ -98,6 +105,10 @@ def ws_gemm_abi_version() -> int:
 
 def ws_gemm_status_str(status: int) -> str:
     return _lib.ws_gemm_status_str(status).decode()
+
+
+def ws_gemm_last_error() -> str:
+    return _lib.ws_gemm_last_error().decode()
 
 
 def ws_gemm_plan(M, N, K, cfg: ws_gemm_config, num_cus: int, wgs_per_cu: int = 0):
@@ -144,7 +155,8 @@ def ws_gemm_destroy(h) -> int:
 
 class WsGemmError(RuntimeError):
     def __init__(self, where: str, status: int):
-        super().__init__("%s: %s (status %d)" % (where, ws_gemm_status_str(status), status))
+        detail = (" [%s]" % ws_gemm_last_error()) if status == WS_ERR_HIP else ""
+        super().__init__("%s: %s (status %d)%s" % (where, ws_gemm_status_str(status), status, detail))
         self.status = status
 
 
