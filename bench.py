@@ -24,7 +24,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 WORKLOAD = "gemm_8192x8192x8192_bf16_normal"
-DEFAULT_POINT = (256, 128, 64, 3, 4, 4)   # (TM, TN, TK, stages, producer waves, consumer waves)
+DEFAULT_POINT = (128, 256, 64, 3, 4, 4)   # (TM, TN, TK, stages, producer waves, consumer waves)
+DEFAULT_LOAD_PATH = "registers"
 PEAK_TFLOPS = 2500.0                      # MI355X dense bf16 MFMA
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 
@@ -81,6 +82,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--point", default=None, help="TMxTNxTKxSTAGESxNPxNC")
+    ap.add_argument("--load-path", default=DEFAULT_LOAD_PATH, choices=("registers", "dma"))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     a = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -105,7 +107,7 @@ def main():
     Ad, Bd = A.cuda(), B.cuda()
     del A, B
     C = torch.empty((wl.M, wl.N), dtype=torch.float32, device="cuda")
-    g = w.WsGemm(wl.M, wl.N, wl.K, (tm, tn, tk), stages, np_, nc, wl.dtype)
+    g = w.WsGemm(wl.M, wl.N, wl.K, (tm, tn, tk), stages, np_, nc, wl.dtype, a.load_path)
     stream = torch.cuda.current_stream()
     a_p, b_p, c_p, s_p = Ad.data_ptr(), Bd.data_ptr(), C.data_ptr(), stream.cuda_stream
 
@@ -120,7 +122,7 @@ def main():
     sm = summary(dev)
     value = wl.flops / (wall_ms * 1e-3) / 1e12
     achieved = wl.flops / (sm["mean_ms"] * 1e-3) / 1e12
-    pkey = "x".join(map(str, point))
+    pkey = "x".join(map(str, point)) + "/" + a.load_path
     out = {
         "metric": "bf16 GEMM TFLOP/s at 8192^3 (fraction of dense MFMA peak in pct_mfma_peak)",
         "value": round(value, 2),
@@ -138,7 +140,7 @@ def main():
         "config": {"workload": wl.name, "M": wl.M, "N": wl.N, "K": wl.K,
                    "tile": [tm, tn, tk], "stages": stages, "producer_waves": np_,
                    "consumer_waves": nc, "split": "%d:1" % (np_ // nc),
-                   "grid": g.info.grid, "rounds": g.info.rounds},
+                   "load_path": a.load_path, "grid": g.info.grid, "rounds": g.info.rounds},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS, 4),
                      "traffic": traffic_for(pkey),

@@ -40,7 +40,7 @@
 extern "C" {
 #endif
 
-#define WS_GEMM_ABI_VERSION 1
+#define WS_GEMM_ABI_VERSION 2
 
 typedef struct ws_gemm_handle* ws_gemm_t; /* opaque handle */
 
@@ -56,12 +56,20 @@ typedef enum {
   WS_ERR_NOT_DIVISIBLE = 6  /* T_M does not divide M, T_N does not divide N or T_K does not divide K */
 } ws_status;
 
+/* How producer waves move a tile from global memory into its LDS slot. */
+typedef enum {
+  WS_LOAD_REGISTERS = 0, /* global_load_dwordx4 into VGPRs several K-iterations ahead, then
+                            ds_write_b128 once the slot is free (more bytes in flight) */
+  WS_LOAD_DMA = 1        /* global_load_lds_dwordx4 straight into the slot once it is free */
+} ws_load_path;
+
 typedef struct {
   int32_t tile_m, tile_n, tile_k; /* (T_M, T_N, T_K): powers of two, 32..256 (tile_k 32..128) */
   int32_t producer_waves;         /* DMA wavefronts per workgroup: consumer_waves or 2x that */
   int32_t consumer_waves;         /* MATH wavefronts per workgroup: 1 or 4 (one per SIMD) */
   int32_t stages;                 /* circular-buffer slots, 2..8 */
   int32_t dtype;                  /* ws_dtype of A and B */
+  int32_t load_path;              /* ws_load_path of the producers */
 } ws_gemm_config;
 
 typedef struct {
@@ -127,6 +135,19 @@ ws_status ws_gemm_query(ws_gemm_t h, ws_gemm_plan_info* out);
  * runs (NULL restores the defaults).  Delays force the buffer-full and
  * buffer-empty waits of Section 2.2; a tiny poll limit forces a timeout. */
 ws_status ws_gemm_set_debug(ws_gemm_t h, const ws_gemm_debug* dbg);
+
+/* Event trace of later runs (Section 2.2's events S_a, S_b, S_m, measured).
+ * `buffer` is caller-owned device memory of at least wgs * iters * 8 * 4
+ * bytes; workgroups 0 .. wgs-1 (wgs <= plan grid) each write iters records
+ * of 8 uint32 shader-clock stamps (low 32 bits) per K-iteration q they
+ * process, in order:
+ *   0 A-tile issue start  1 B-tile issue start  2 A landed  3 B landed
+ *   4 consumer sees slot full  5 consumer MFMA start  6 slot released
+ *   7 epilogue end (last K-iteration of a tile; otherwise left untouched).
+ * Records beyond the iterations a workgroup runs are left untouched.
+ * NULL buffer turns tracing off.  Tracing costs a few instructions per
+ * K-iteration in the traced workgroups. */
+ws_status ws_gemm_set_trace(ws_gemm_t h, void* buffer, int64_t bytes, int32_t wgs, int32_t iters);
 
 /* Free the handle; NULL is a no-op.  Must not race with runs using it. */
 ws_status ws_gemm_destroy(ws_gemm_t h);

@@ -75,7 +75,31 @@ struct KernelArgs {
   int32_t producer_delay;  // debug: s_sleep bursts per K-iteration in producers
   int32_t consumer_delay;  // debug: s_sleep bursts per K-iteration in consumers
   int32_t* err;            // set to 1 when a bounded wait gives up
+  uint32_t* trace;         // event trace (null: off), [trace_wgs][trace_iters][kTraceEvents]
+  int32_t trace_wgs;       // workgroups 0 .. trace_wgs-1 are traced
+  int32_t trace_iters;     // K-iterations recorded per workgroup
+  int32_t load_path;       // producer load path: 0 register-staged, 1 LDS-DMA
 };
+
+// Event trace: one record of kTraceEvents 32-bit shader-clock stamps per
+// K-iteration q of a traced workgroup (the paper's event analysis, Section
+// 2.2: S_a(i), S_b(i), S_m(i)).
+//   0  producer starts issuing the A tile of q            (S_a)
+//   1  producer starts issuing the B tile of q            (S_b)
+//   2  the A tile of q has landed in LDS (signal)
+//   3  the B tile of q has landed in LDS (signal)
+//   4  consumer wave 0 observes slot q full
+//   5  consumer wave 0 starts the MFMAs of q              (S_m)
+//   6  consumer wave 0 releases slot q
+//   7  consumer wave 0 finished the epilogue (last K-iteration of a tile), else 0
+constexpr int kTraceEvents = 8;
+// LDS header words holding the producer stamps of each slot (indices 24..55).
+constexpr int kStampIssueA = 24, kStampIssueB = 32, kStampLandA = 40, kStampLandB = 48;
+
+// Low 32 bits of the shader-clock counter (s_memtime).
+__device__ __forceinline__ uint32_t cycles32() {
+  return (uint32_t)__builtin_amdgcn_s_memtime();
+}
 
 // XOR swizzle of the 16-byte chunks of A-tile row r.  It depends on r & 31
 // only, so rows 32 apart share it and the consumer can fold whole 32-row
@@ -116,19 +140,25 @@ __device__ __forceinline__ void wait_vmcnt() {
 // signal(): add one to an LDS counter from lane 0 only, after every earlier
 // LDS access of this wave has completed.  Done in one asm block with the exec
 // mask narrowed to lane 0, so the surrounding code stays branch-free.
+// YOUNGER: how many of this wave's most recent LDS operations may still be
+// outstanding (LDS operations of a wave complete in order, so every older
+// one has completed).  The caller guarantees no scalar-memory load is in
+// flight, since those would share the counter out of order.
+template <int YOUNGER = 0>
 __device__ __forceinline__ void lds_signal(WSG_LDS uint32_t* p) {
+  static_assert(YOUNGER >= 0 && YOUNGER <= 15, "lgkmcnt range");
 #if defined(__HIP_DEVICE_COMPILE__)
   const uint32_t addr = (uint32_t)(uintptr_t)p;
   const uint32_t one = 1u;
   uint64_t saved;
   asm volatile(
-      "s_waitcnt lgkmcnt(0)\n\t"
+      "s_waitcnt lgkmcnt(%3)\n\t"
       "s_mov_b64 %0, exec\n\t"
       "s_mov_b64 exec, 1\n\t"
       "ds_add_u32 %1, %2\n\t"
       "s_mov_b64 exec, %0"
       : "=&s"(saved)
-      : "v"(addr), "v"(one)
+      : "v"(addr), "v"(one), "n"(YOUNGER)
       : "memory");
 #endif
 }
@@ -152,34 +182,58 @@ __device__ __forceinline__ uint32_t lds_read_now(WSG_LDS uint32_t* p) {
 #endif
 }
 
-// wait(): poll *ctr until it reaches target (wrap-safe).  Returns false when
-// the workgroup aborted or this wait exceeded the poll limit (it then raises
-// the abort flag and the global error word, so every wave drains quickly).
-// The result is wave-uniform.
+// Store a wave-uniform value to an LDS word from lane 0 (asm, so the producer's
+// vmcnt accounting and the compiler's LDS ordering are untouched).
+__device__ __forceinline__ void lds_stamp(WSG_LDS uint32_t* p, uint32_t value) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const uint32_t addr = (uint32_t)(uintptr_t)p;
+  uint64_t saved;
+  asm volatile(
+      "s_mov_b64 %0, exec\n\t"
+      "s_mov_b64 exec, 1\n\t"
+      "ds_write_b32 %1, %2\n\t"
+      "s_mov_b64 exec, %0"
+      : "=&s"(saved)
+      : "v"(addr), "v"(value)
+      : "memory");
+#endif
+}
+
+// wait(): poll *ctr until it reaches target (wrap-safe).  Returns true when
+// it did; false when the workgroup aborted or this wait exceeded the poll
+// limit (it then raises the workgroup abort flag and the device error word,
+// so every wave drains quickly).  The result is wave-uniform.  The poll loop
+// itself issues no vector-memory instruction, so it does not disturb the
+// compiler's accounting of outstanding loads around it.
+__device__ __forceinline__ void report_timeout(WSG_LDS uint32_t* abort_flag, int32_t* err) {
+  if ((threadIdx.x & 63) == 0) {
+    __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
 __device__ __forceinline__ bool wait_counter(WSG_LDS uint32_t* ctr, uint32_t target,
                                              WSG_LDS uint32_t* abort_flag, int spin_limit,
                                              int32_t* err) {
   int spins = 0;
-  bool ok = true;
+  int status = 0;  // 0 reached, 1 aborted elsewhere, 2 timed out here
   while (true) {
     const uint32_t v = lds_read_now(ctr);
     if ((int32_t)(v - target) >= 0) break;
     if (lds_read_now(abort_flag)) {
-      ok = false;
+      status = 1;
       break;
     }
     if (++spins > spin_limit) {
-      if ((threadIdx.x & 63) == 0) {
-        __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-      ok = false;
+      status = 2;
       break;
     }
     __builtin_amdgcn_s_sleep(1);
   }
   compiler_fence();
-  return __builtin_amdgcn_readfirstlane((int)ok) != 0;
+  status = __builtin_amdgcn_readfirstlane(status);
+  if (status == 2) report_timeout(abort_flag, err);
+  return status == 0;
 }
 
 __device__ __forceinline__ void debug_delay(int n) {
@@ -233,10 +287,28 @@ __device__ __forceinline__ int first_slot(const KernelArgs& args) {
 // ---------------------------------------------------------------------------
 // Producer (DMA warp).  Waits for a free slot, streams its share of the A
 // and/or B tile of one K-iteration into that slot, and signals the slot full
-// once the data has landed.  The data of K-iteration q is awaited only after
-// the loads of q + 1 are issued, so two K-iterations are in flight per wave.
+// once the data has landed.  Up to `lag` + 1 K-iterations are in flight per
+// wave: iteration q is signalled once iteration q + lag has been issued.
+// Before blocking on a slot that is still in use, every pending iteration is
+// published (oldest first), so a consumer never waits on data that landed.
 // ---------------------------------------------------------------------------
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool DO_A, bool DO_B>
+
+// Block until at most n of this wave's most recent K-iterations (LOADS DMA
+// instructions each) are still in flight.
+template <int LOADS>
+__device__ __forceinline__ void wait_landed(uint32_t n) {
+  switch (n) {
+    case 0: wait_vmcnt<0>(); break;
+    case 1: wait_vmcnt<(LOADS * 1 <= 63 ? LOADS * 1 : 0)>(); break;
+    case 2: wait_vmcnt<(LOADS * 2 <= 63 ? LOADS * 2 : 0)>(); break;
+    case 3: wait_vmcnt<(LOADS * 3 <= 63 ? LOADS * 3 : 0)>(); break;
+    case 4: wait_vmcnt<(LOADS * 4 <= 63 ? LOADS * 4 : 0)>(); break;
+    case 5: wait_vmcnt<(LOADS * 5 <= 63 ? LOADS * 5 : 0)>(); break;
+    default: wait_vmcnt<(LOADS * 6 <= 63 ? LOADS * 6 : 0)>(); break;
+  }
+}
+
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B>
 __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS char* smem,
                                               int a_rank, int b_rank, int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
@@ -245,18 +317,19 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
   constexpr int A_PER = DO_A ? G::A_INSTR / A_GROUP : 0;     // DMA instructions per wave
   constexpr int B_PER = DO_B ? G::B_INSTR / B_GROUP : 0;
   constexpr int LOADS = A_PER + B_PER;
+  constexpr int MAX_LAG = (63 / LOADS) < 6 ? (63 / LOADS) : 6;
   static_assert(G::A_INSTR % A_GROUP == 0 && G::B_INSTR % B_GROUP == 0, "even DMA split");
-  static_assert(LOADS > 0 && LOADS <= 63, "vmcnt range");
+  static_assert(LOADS > 0 && MAX_LAG >= 1, "vmcnt range");
 
   WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
   WSG_LDS uint32_t* empty = full + kMaxStages;
   WSG_LDS uint32_t* abort_flag = full + 2 * kMaxStages;
   const int K = args.K, N = args.N;
 
-  // Element offset, inside the tile, of the 16-byte chunk this lane fetches for
+  // Byte offset, inside the tile, of the 16-byte chunk this lane fetches for
   // each of its DMA instructions (the LDS side is fixed: lane l writes bytes
   // 16 l .. 16 l + 15 of the instruction's KiB).
-  uint32_t a_goff[A_PER > 0 ? A_PER : 1];  // bytes
+  uint32_t a_goff[A_PER > 0 ? A_PER : 1];
   uint32_t b_goff[B_PER > 0 ? B_PER : 1];
 #pragma unroll
   for (int n = 0; n < A_PER; ++n) {
@@ -272,11 +345,22 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
     b_goff[n] = (uint32_t)((kq * 4 + (w >> 1)) * N + nq * 16 + (w & 1) * 8) * 2u;
   }
 
+  const bool tracing = TRACE && args.trace != nullptr && (int)blockIdx.x < args.trace_wgs;
+  // signal(): data of the slot has landed; stamp its landing time first when tracing.
+  auto publish = [&](uint32_t pslot) {
+    if (tracing) {
+      const uint32_t t = cycles32();
+      if (DO_A && a_rank == 0) lds_stamp(&full[kStampLandA + pslot], t);
+      if (DO_B && b_rank == 0) lds_stamp(&full[kStampLandB + pslot], t);
+    }
+    lds_signal(&full[pslot]);
+  };
   const int Gd = gridDim.x;
   const uint32_t P = (uint32_t)args.stages;
-  uint32_t q = 0;
-  bool pending = false;
-  uint32_t pending_slot = 0;
+  uint32_t lag = P > 3 ? P - 2 : 1;
+  if (lag > (uint32_t)MAX_LAG) lag = MAX_LAG;
+  uint32_t q = 0;      // next K-iteration to issue
+  uint32_t q_sig = 0;  // next K-iteration to signal
   for (int v = first_slot(args); v < args.num_tiles; v += Gd) {
     int ti, tj;
     tile_coords(v, args.tiles_m, args.tiles_n, args.group_m, &ti, &tj);
@@ -289,10 +373,10 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
         // wait(): the slot is free once every consumer wave released use - 1.
         const uint32_t need = use * NC;
         if ((int32_t)(lds_read_now(&empty[slot]) - need) < 0) {
-          if (pending) {  // publish the previous K-iteration before blocking
-            wait_vmcnt<0>();
-            lds_signal(&full[pending_slot]);
-            pending = false;
+          while (q_sig < q) {  // publish pending iterations first, oldest first
+            wait_landed<LOADS>(q - q_sig - 1);
+            publish(q_sig % P);
+            ++q_sig;
           }
           if (!wait_counter(&empty[slot], need, abort_flag, args.spin_limit, args.err)) {
             wait_vmcnt<0>();  // no DMA into LDS may outlive the wave
@@ -302,6 +386,7 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
       }
       if (args.producer_delay) debug_delay(args.producer_delay);
       compiler_fence();
+      if (tracing && a_rank == 0 && DO_A) lds_stamp(&full[kStampIssueA + slot], cycles32());
       WSG_LDS char* a_dst = smem + kHeaderBytes + slot * G::STAGE;
       WSG_LDS char* b_dst = a_dst + G::A_BYTES;
       if constexpr (DO_A) {
@@ -313,6 +398,7 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
                                            16, 0, 0);
       }
       if constexpr (DO_B) {
+        if (tracing && b_rank == 0) lds_stamp(&full[kStampIssueB + slot], cycles32());
         const char* src = (const char*)(b_tile + (int64_t)kk * TK * N);
 #pragma unroll
         for (int n = 0; n < B_PER; ++n)
@@ -320,31 +406,176 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
                                            (WSG_LDS void*)(b_dst + (b_rank + n * B_GROUP) * 1024),
                                            16, 0, 0);
       }
-      if (pending) {  // signal(): K-iteration q - 1 has landed
-        wait_vmcnt<LOADS>();
-        lds_signal(&full[pending_slot]);
+      // signal(): iteration q - lag has landed once at most `lag` newer ones are in flight.
+      if (q + 1 - q_sig > lag) {
+        wait_landed<LOADS>(lag);
+        publish(q_sig % P);
+        ++q_sig;
       }
-      pending = true;
-      pending_slot = slot;
     }
   }
-  if (pending) {
-    wait_vmcnt<0>();
-    lds_signal(&full[pending_slot]);
+  while (q_sig < q) {
+    wait_landed<LOADS>(q - q_sig - 1);
+    publish(q_sig % P);
+    ++q_sig;
   }
 }
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16>
+// ---------------------------------------------------------------------------
+// Register-staged producer (DMA warp).  The wave loads its share of the tiles
+// of K-iteration q + L into VGPRs (global_load_dwordx4) while K-iteration q
+// waits in registers for its slot; once the slot is free it writes q with
+// ds_write_b128 and signals.  Bytes in flight per wave are L iterations'
+// worth, independent of the LDS ring depth: producer waves get the kernel's
+// full VGPR allocation (sized for the consumers) and would otherwise leave
+// it idle.  The LDS layout is the one the LDS-DMA producer writes.
+// ---------------------------------------------------------------------------
+typedef __attribute__((ext_vector_type(4))) int i32x4_t;
+
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B>
+__device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LDS char* smem,
+                                                  int a_rank, int b_rank, int lane) {
+  using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
+  constexpr int A_GROUP = (SPLIT == 1) ? G::NP : G::NP / 2;
+  constexpr int B_GROUP = (SPLIT == 1) ? G::NP : G::NP / 2;
+  constexpr int A_PER = DO_A ? G::A_INSTR / A_GROUP : 0;
+  constexpr int B_PER = DO_B ? G::B_INSTR / B_GROUP : 0;
+  constexpr int LOADS = A_PER + B_PER;
+  constexpr int STAGE_VGPRS = (G::NW <= 8) ? 152 : 96;
+  constexpr int L0 = STAGE_VGPRS / (4 * LOADS);
+  constexpr int L1 = (63 / LOADS) < L0 ? (63 / LOADS) : L0;
+  constexpr int L = L1 < 1 ? 1 : (L1 > 6 ? 6 : L1);  // K-iterations staged in VGPRs
+  static_assert(G::A_INSTR % A_GROUP == 0 && G::B_INSTR % B_GROUP == 0, "even split");
+
+  WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
+  WSG_LDS uint32_t* empty = full + kMaxStages;
+  WSG_LDS uint32_t* abort_flag = full + 2 * kMaxStages;
+  const int K = args.K, N = args.N;
+
+  uint32_t goff[LOADS];  // byte offset of this lane's 16-byte chunk in the A / B tile
+#pragma unroll
+  for (int n = 0; n < A_PER; ++n) {
+    const int q = (a_rank + n * A_GROUP) * 64 + lane;
+    const int r = q / G::CA, p = q % G::CA;
+    goff[n] = (uint32_t)(r * K + 8 * (p ^ swz_a<TK>(r))) * 2u;
+  }
+#pragma unroll
+  for (int n = 0; n < B_PER; ++n) {
+    const int q = (b_rank + n * B_GROUP) * 64 + lane;
+    const int blk = q >> 3, w = q & 7;
+    const int kq = blk / G::NQ, nq = blk % G::NQ;
+    goff[A_PER + n] = (uint32_t)((kq * 4 + (w >> 1)) * N + nq * 16 + (w & 1) * 8) * 2u;
+  }
+  const uint32_t lane16 = (uint32_t)lane * 16u;
+
+  const bool tracing = TRACE && args.trace != nullptr && (int)blockIdx.x < args.trace_wgs;
+  const int Gd = gridDim.x;
+  const int g0 = first_slot(args);
+  const int my_tiles = (args.num_tiles - g0 + Gd - 1) / Gd;
+  const uint32_t S = (uint32_t)args.iters;
+  const uint32_t total = (uint32_t)my_tiles * S;
+  const uint32_t P = (uint32_t)args.stages;
+
+  // Issue cursor: the next K-iteration whose loads go out.
+  int v_i = g0, ti_i = 0, tj_i = 0;
+  uint32_t kk_i = 0, q_iss = 0;
+  tile_coords(v_i, args.tiles_m, args.tiles_n, args.group_m, &ti_i, &tj_i);
+
+  i32x4_t stage[L][LOADS];
+  uint32_t t_issue[L];
+  // Loads go out unconditionally (past the last K-iteration they re-read the
+  // last valid tile and are never written to LDS), so every path through the
+  // loop has the same number of loads in flight and the compiler's vmcnt
+  // waits before each ds_write allow exactly L - 1 newer iterations.
+  auto issue = [&](int u) {
+    if (tracing) t_issue[u] = cycles32();
+    const char* a_src = (const char*)(args.A + (int64_t)ti_i * TM * K + kk_i * TK);
+    const char* b_src = (const char*)(args.B + (int64_t)kk_i * TK * N + (int64_t)tj_i * TN);
+#pragma unroll
+    for (int n = 0; n < A_PER; ++n) stage[u][n] = *(const i32x4_t*)(a_src + goff[n]);
+#pragma unroll
+    for (int n = 0; n < B_PER; ++n)
+      stage[u][A_PER + n] = *(const i32x4_t*)(b_src + goff[A_PER + n]);
+    if (q_iss + 1 < total) {
+      ++q_iss;
+      if (++kk_i == S) {
+        kk_i = 0;
+        v_i += Gd;
+        tile_coords(v_i, args.tiles_m, args.tiles_n, args.group_m, &ti_i, &tj_i);
+      }
+    }
+  };
+
+#pragma unroll
+  for (int u = 0; u < L; ++u) issue(u);
+
+  for (uint32_t q0 = 0; q0 < total; q0 += L) {
+#pragma unroll
+    for (int u = 0; u < L; ++u) {
+      const uint32_t q = q0 + u;
+      if (q < total) {
+      const uint32_t slot = q % P;
+      const uint32_t use = q / P;
+      if (use > 0) {
+        const uint32_t need = use * NC;
+        if ((int32_t)(lds_read_now(&empty[slot]) - need) < 0) {
+          if (!wait_counter(&empty[slot], need, abort_flag, args.spin_limit, args.err)) {
+            wait_vmcnt<0>();
+            return;
+          }
+        }
+      }
+      if (args.producer_delay) debug_delay(args.producer_delay);
+      compiler_fence();
+      WSG_LDS char* base = smem + kHeaderBytes + slot * G::STAGE + lane16;
+#pragma unroll
+      for (int n = 0; n < A_PER; ++n)
+        *(WSG_LDS i32x4_t*)(base + (a_rank + n * A_GROUP) * 1024) = stage[u][n];
+#pragma unroll
+      for (int n = 0; n < B_PER; ++n)
+        *(WSG_LDS i32x4_t*)(base + G::A_BYTES + (b_rank + n * B_GROUP) * 1024) = stage[u][A_PER + n];
+      if (tracing) {
+        const uint32_t t = cycles32();
+        if (DO_A && a_rank == 0) {
+          lds_stamp(&full[kStampIssueA + slot], t_issue[u]);
+          lds_stamp(&full[kStampLandA + slot], t);
+        }
+        if (DO_B && b_rank == 0) {
+          lds_stamp(&full[kStampIssueB + slot], t_issue[u]);
+          lds_stamp(&full[kStampLandB + slot], t);
+        }
+      }
+      lds_signal(&full[slot]);  // waits for the LDS writes, then signals
+      }
+      issue(u);  // refill this register stage with K-iteration q + L
+    }
+  }
+  wait_vmcnt<0>();
+}
+
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE>
 __device__ __forceinline__ void producer(const KernelArgs& args, WSG_LDS char* smem, int pw,
                                          int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
-  if constexpr (SPLIT == 1) {
-    producer_loop<TM, TN, TK, NC, SPLIT, BF16, true, true>(args, smem, pw, pw, lane);
+  // Load path (wave-uniform): 0 = register-staged, 1 = LDS-DMA.
+  if (args.load_path == 1) {
+    if constexpr (SPLIT == 1) {
+      producer_loop<TM, TN, TK, NC, SPLIT, BF16, TRACE, true, true>(args, smem, pw, pw, lane);
+    } else {
+      if (pw < G::NP / 2)
+        producer_loop<TM, TN, TK, NC, SPLIT, BF16, TRACE, true, false>(args, smem, pw, 0, lane);
+      else
+        producer_loop<TM, TN, TK, NC, SPLIT, BF16, TRACE, false, true>(args, smem, 0, pw - G::NP / 2, lane);
+    }
   } else {
-    if (pw < G::NP / 2)
-      producer_loop<TM, TN, TK, NC, SPLIT, BF16, true, false>(args, smem, pw, 0, lane);
-    else
-      producer_loop<TM, TN, TK, NC, SPLIT, BF16, false, true>(args, smem, 0, pw - G::NP / 2, lane);
+    if constexpr (SPLIT == 1) {
+      producer_loop_reg<TM, TN, TK, NC, SPLIT, BF16, TRACE, true, true>(args, smem, pw, pw, lane);
+    } else {
+      if (pw < G::NP / 2)
+        producer_loop_reg<TM, TN, TK, NC, SPLIT, BF16, TRACE, true, false>(args, smem, pw, 0, lane);
+      else
+        producer_loop_reg<TM, TN, TK, NC, SPLIT, BF16, TRACE, false, true>(args, smem, 0, pw - G::NP / 2, lane);
+    }
   }
 }
 
@@ -388,19 +619,24 @@ struct ConsumerOps {
   }
 };
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16>
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE>
 __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* smem, int cw,
                                          int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
   using Ops = ConsumerOps<TM, TN, TK, NC, SPLIT, BF16>;
   static_assert(G::KS % 2 == 0, "k-steps per K-iteration must be even");
+  // Operand prefetch distance in k-steps, and fragment buffers (buffer of
+  // k-step s is s % NB, the same in every K-iteration).
+  constexpr int D = (G::KS >= 4) ? 3 : 1;
+  constexpr int NB = (D == 1) ? 2 : G::KS;
+  static_assert(NB >= D + 1 && G::KS % NB == 0, "fragment buffers must cover the prefetch");
   WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
   WSG_LDS uint32_t* empty = full + kMaxStages;
   WSG_LDS uint32_t* abort_flag = full + 2 * kMaxStages;
 
   const int wm = cw / G::WGN, wn = cw % G::WGN;
   // A: lane reads row wm*WM + mb*32 + lane%32, chunk 2s + lane/32 (swizzled;
-  // the swizzle depends on row & 15, hence only on the lane).
+  // the swizzle repeats every 32 rows, so it depends only on the lane).
   uint32_t a_off[G::KS];
   {
     const int r = wm * G::WM + (lane & 31);
@@ -433,53 +669,101 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
 #pragma unroll
     for (int nb = 0; nb < G::BN; ++nb) acc[mb][nb] = f32x16_t{};
 
-  i16x8_t fa[2][G::BM];
-  i16x8_t fb[2][G::BN];
+  i16x8_t fa[NB][G::BM];
+  i16x8_t fb[NB][G::BN];
 
-  // Prologue: wait for K-iteration 0 and read its first k-step.
+  // Event trace (consumer wave 0 of traced workgroups writes the records).
+  const bool tracing = TRACE && args.trace != nullptr && cw == 0 && (int)blockIdx.x < args.trace_wgs;
+  uint32_t* trec = tracing ? args.trace + (size_t)blockIdx.x * args.trace_iters * kTraceEvents : nullptr;
+  auto record = [&](uint32_t iq, int ev, uint32_t value) {
+    if (tracing && iq < (uint32_t)args.trace_iters && lane == 0) trec[iq * kTraceEvents + ev] = value;
+  };
+  // Slot `ps` of K-iteration iq is full: copy the producer stamps, stamp "ready".
+  auto record_ready = [&](uint32_t iq, uint32_t ps) {
+    if (tracing) {
+      const uint32_t t = cycles32();
+      record(iq, 0, lds_read_now(&full[kStampIssueA + ps]));
+      record(iq, 1, lds_read_now(&full[kStampIssueB + ps]));
+      record(iq, 2, lds_read_now(&full[kStampLandA + ps]));
+      record(iq, 3, lds_read_now(&full[kStampLandB + ps]));
+      record(iq, 4, t);
+    }
+  };
+
+  // Prologue: wait for K-iteration 0 and read its first D k-steps.
   if (!wait_counter(&full[0], (uint32_t)G::NP, abort_flag, args.spin_limit, args.err)) return;
-  Ops::load(fa[0], fb[0], smem + kHeaderBytes, smem + kHeaderBytes + G::A_BYTES, a_off[0], b_off,
-            0);
+  record_ready(0, 0);
+#pragma unroll
+  for (int s = 0; s < D; ++s)
+    Ops::load(fa[s], fb[s], smem + kHeaderBytes, smem + kHeaderBytes + G::A_BYTES, a_off[s],
+              b_off, s);
 
+  constexpr int RA = G::KS - D;  // region that acquires the next slot
+  constexpr int RR = RA + 1;      // region that releases the current slot
+  static_assert(RA >= 1, "the next slot is peeked one region before it is acquired");
+  uint32_t rel_slot = 0;
+  bool rel_pending = false;
   uint32_t q = 0, kk = 0;
   while (true) {
     const uint32_t slot = q % P;
     WSG_LDS char* a_src = smem + kHeaderBytes + slot * G::STAGE;
     WSG_LDS char* b_src = a_src + G::A_BYTES;
     const bool has_next = (q + 1) < total;
-    const uint32_t nslot = (q + 1) % P;
+    const uint32_t nslot = has_next ? (q + 1) % P : slot;
     const uint32_t ntarget = ((q + 1) / P + 1) * (uint32_t)G::NP;
+    WSG_LDS char* na_src = smem + kHeaderBytes + nslot * G::STAGE;
+    WSG_LDS char* nb_src = na_src + G::A_BYTES;
     uint32_t peek = 0;
     if (args.consumer_delay) debug_delay(args.consumer_delay);
+    if (tracing) record(q, 5, cycles32());
 
-    // k-steps 0 .. KS-2: read step s+1, multiply step s.  The scheduling
-    // barriers keep each step's MFMAs ahead of the next step's reads.
+    // Region s: read the operands of k-step s + D, multiply k-step s.
+    //   region RA = KS - D: wait() for slot q+1 (peeked one region earlier,
+    //     before that region's reads), then read its first k-step;
+    //   region RR = RA + 1: signal() slot q free, waiting only for the reads
+    //     older than region RA's (RR == KS: region 0 of the next K-iteration).
 #pragma unroll
-    for (int s = 0; s + 1 < G::KS; ++s) {
-      Ops::load(fa[(s + 1) & 1], fb[(s + 1) & 1], a_src, b_src, a_off[s + 1], b_off, s + 1);
-      if (s + 2 == G::KS) peek = lds_peek(&full[nslot]);
-      Ops::mma(acc, fa[s & 1], fb[s & 1]);
-      // issue order inside the step: all LDS reads, then the MFMAs
-      if (s + 2 == G::KS)
-        __builtin_amdgcn_sched_group_barrier(0x100, Ops::kReads + 1, 0);
-      else
+    for (int s = 0; s < G::KS; ++s) {
+      const int tp = s + D;
+      if (RR == G::KS && s == 0 && rel_pending) {
+        lds_signal<Ops::kReads>(&empty[rel_slot]);
+        if (tracing) record(q - 1, 6, cycles32());
+        rel_pending = false;
+      }
+      if (RR < G::KS && s == RR) {
+        lds_signal<Ops::kReads>(&empty[slot]);
+        if (tracing) record(q, 6, cycles32());
+      }
+      if (s == RA) {
+        if (has_next && (int32_t)(__builtin_amdgcn_readfirstlane(peek) - ntarget) < 0) {
+          if (!wait_counter(&full[nslot], ntarget, abort_flag, args.spin_limit, args.err)) return;
+        }
+        compiler_fence();
+        if (tracing && has_next) record_ready(q + 1, nslot);
+      }
+      if (s == RA - 1) {
+        peek = lds_peek(&full[nslot]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (tp < G::KS) {
+        Ops::load(fa[tp % NB], fb[tp % NB], a_src, b_src, a_off[tp], b_off, tp);
+        Ops::mma(acc, fa[s % NB], fb[s % NB]);
         __builtin_amdgcn_sched_group_barrier(0x100, Ops::kReads, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, Ops::kMfma, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, Ops::kMfma, 0);
+      } else {
+        // Unconditional, so the compiler's LDS wait counts stay exact on
+        // every path; after the last K-iteration these re-read the current
+        // slot and are never used.
+        Ops::load(fa[(tp - G::KS) % NB], fb[(tp - G::KS) % NB], na_src, nb_src,
+                  a_off[tp - G::KS], b_off, tp - G::KS);
+        Ops::mma(acc, fa[s % NB], fb[s % NB]);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
-    // signal(): every operand of this K-iteration is in registers.
-    lds_signal(&empty[slot]);
-    if (has_next) {
-      // wait(): the peek was issued one k-step ago; poll only if it was early.
-      if ((int32_t)(__builtin_amdgcn_readfirstlane(peek) - ntarget) < 0) {
-        if (!wait_counter(&full[nslot], ntarget, abort_flag, args.spin_limit, args.err)) return;
-      }
-      compiler_fence();
-      WSG_LDS char* na = smem + kHeaderBytes + nslot * G::STAGE;
-      Ops::load(fa[0], fb[0], na, na + G::A_BYTES, a_off[0], b_off, 0);
+    if (RR == G::KS) {
+      rel_slot = slot;
+      rel_pending = true;
     }
-    Ops::mma(acc, fa[1], fb[1]);
-    __builtin_amdgcn_sched_barrier(0);
     ++q;
     if (++kk == S) {
       // Epilogue: fp32 tile to C.  acc[mb][nb][e] is row 8(e/4) + 4(lane/32) + e%4,
@@ -500,7 +784,14 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
           for (int nb = 0; nb < G::BN; ++nb)
             *(float*)(rowp + lane_off + nb * 128) = acc[mb][nb][e];
         }
-      if (!has_next) break;
+      if (tracing) record(q - 1, 7, cycles32());
+      if (!has_next) {
+        if (RR == G::KS && rel_pending) {  // every slot use is released, the last one too
+          lds_signal<0>(&empty[rel_slot]);
+          if (tracing) record(q - 1, 6, cycles32());
+        }
+        break;
+      }
       kk = 0;
       v += Gd;
       tile_coords(v, args.tiles_m, args.tiles_n, args.group_m, &ti, &tj);
@@ -513,7 +804,7 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
   }
 }
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16>
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE>
 __global__ void __launch_bounds__((NC + NC * SPLIT) * 64) ws_gemm_kernel(KernelArgs args) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
   extern __shared__ __attribute__((aligned(1024))) char smem_generic[];
@@ -523,9 +814,9 @@ __global__ void __launch_bounds__((NC + NC * SPLIT) * 64) ws_gemm_kernel(KernelA
   if (threadIdx.x < 2 * kMaxStages + 1) ((WSG_LDS uint32_t*)smem)[threadIdx.x] = 0u;
   __syncthreads();
   if (wave < NC)
-    consumer<TM, TN, TK, NC, SPLIT, BF16>(args, smem, wave, lane);
+    consumer<TM, TN, TK, NC, SPLIT, BF16, TRACE>(args, smem, wave, lane);
   else
-    producer<TM, TN, TK, NC, SPLIT, BF16>(args, smem, wave - NC, lane);
+    producer<TM, TN, TK, NC, SPLIT, BF16, TRACE>(args, smem, wave - NC, lane);
 }
 
 }  // namespace wsg

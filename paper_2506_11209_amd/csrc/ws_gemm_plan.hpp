@@ -41,7 +41,7 @@ WSG_HD inline int xcd_slot(int g, int G) { return (g & 7) * (G >> 3) + (g >> 3);
 struct PlanIn {
   int64_t M, N, K;
   int32_t tile_m, tile_n, tile_k;
-  int32_t producer_waves, consumer_waves, stages, dtype;
+  int32_t producer_waves, consumer_waves, stages, dtype, load_path;
   int32_t num_cus;     // compute units on the device
   int32_t wgs_per_cu;  // resident workgroups per CU (<= 0: derive from LDS and waves)
 };
@@ -76,6 +76,7 @@ inline int plan_launch(const PlanIn& in, PlanOut* out) {
   if (in.M <= 0 || in.N <= 0 || in.K <= 0) return kPlanInvalid;
   if (in.M > (1 << 30) || in.N > (1 << 30) || in.K > (1 << 30)) return kPlanInvalid;
   if (in.dtype != 0 && in.dtype != 1) return kPlanInvalid;
+  if (in.load_path != 0 && in.load_path != 1) return kPlanInvalid;
   if (!is_pow2_in(in.tile_m, 32, 256) || !is_pow2_in(in.tile_n, 32, 256) ||
       !is_pow2_in(in.tile_k, 32, 128))
     return kPlanInvalid;

@@ -32,12 +32,13 @@ def point_key(p):
     return "x".join(str(x) for x in p)
 
 
-def measure_point(wl, point, Ad, Bd, C, steps, warmup):
+def measure_point(wl, point, Ad, Bd, C, steps, warmup, load_path="registers"):
     tm, tn, tk, stages, np_, nc = point
-    cfg = w.config((tm, tn, tk), stages, np_, nc, wl.dtype)
+    cfg = w.config((tm, tn, tk), stages, np_, nc, wl.dtype, load_path)
     s, h = w.ws_gemm_create(wl.M, wl.N, wl.K, cfg)
     rec = {"workload": wl.name, "tile": [tm, tn, tk], "stages": stages, "producer_waves": np_,
-           "consumer_waves": nc, "split": "%d:1" % (np_ // nc), "point": point_key(point)}
+           "consumer_waves": nc, "split": "%d:1" % (np_ // nc), "load_path": load_path,
+           "point": point_key(point) + "/" + load_path}
     if s != w.WS_OK:
         rec["status"] = w.ws_gemm_status_str(s)
         return rec
@@ -75,6 +76,8 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--out", default=None)
+    ap.add_argument("--load-paths", default="registers,dma",
+                    help="comma-separated producer load paths to sweep (registers, dma)")
     ap.add_argument("--points", default=None,
                     help="comma-separated TMxTNxTKxSTAGESxNPxNC list (default: the workload's)")
     a = ap.parse_args(argv)
@@ -96,15 +99,17 @@ def main(argv=None):
     C = torch.empty((wl.M, wl.N), dtype=torch.float32, device="cuda")
     del A, B
     for p in points:
-        if point_key(p) in done:
-            continue
-        print("sweep point %s" % point_key(p), file=sys.stderr, flush=True)
-        rec = measure_point(wl, p, Ad, Bd, C, a.steps, a.warmup)
-        line = json.dumps(rec)
-        print(line, flush=True)
-        if a.out:
-            with open(a.out, "a") as f:
-                f.write(line + "\n")
+        for lp in a.load_paths.split(","):
+            key = point_key(p) + "/" + lp
+            if key in done:
+                continue
+            print("sweep point %s" % key, file=sys.stderr, flush=True)
+            rec = measure_point(wl, p, Ad, Bd, C, a.steps, a.warmup, lp)
+            line = json.dumps(rec)
+            print(line, flush=True)
+            if a.out:
+                with open(a.out, "a") as f:
+                    f.write(line + "\n")
 
 
 if __name__ == "__main__":

@@ -26,6 +26,8 @@ if not os.path.exists(LIBRARY):
 _lib = ctypes.CDLL(LIBRARY)
 
 WS_F16, WS_BF16 = 0, 1
+WS_LOAD_REGISTERS, WS_LOAD_DMA = 0, 1
+LOAD_PATHS = {"registers": WS_LOAD_REGISTERS, "dma": WS_LOAD_DMA}
 DTYPE_CODES = {"f16": WS_F16, "bf16": WS_BF16}
 
 WS_OK = 0
@@ -40,7 +42,8 @@ WS_ERR_NOT_DIVISIBLE = 6
 class ws_gemm_config(ctypes.Structure):
     _fields_ = [("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32), ("tile_k", ctypes.c_int32),
                 ("producer_waves", ctypes.c_int32), ("consumer_waves", ctypes.c_int32),
-                ("stages", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+                ("stages", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("load_path", ctypes.c_int32)]
 
 
 class ws_gemm_plan_info(ctypes.Structure):
@@ -84,6 +87,8 @@ _lib.ws_gemm_query.argtypes = [_h, ctypes.POINTER(ws_gemm_plan_info)]
 _lib.ws_gemm_query.restype = _i32
 _lib.ws_gemm_set_debug.argtypes = [_h, ctypes.POINTER(ws_gemm_debug)]
 _lib.ws_gemm_set_debug.restype = _i32
+_lib.ws_gemm_set_trace.argtypes = [_h, _p, _i64, _i32, _i32]
+_lib.ws_gemm_set_trace.restype = _i32
 _lib.ws_gemm_destroy.argtypes = [_h]
 _lib.ws_gemm_destroy.restype = _i32
 
@@ -92,9 +97,11 @@ def library() -> ctypes.CDLL:
     return _lib
 
 
-def config(tile=(128, 128, 32), stages=3, producer_waves=4, consumer_waves=4, dtype="bf16"):
+def config(tile=(128, 128, 32), stages=3, producer_waves=4, consumer_waves=4, dtype="bf16",
+           load_path="registers"):
     tm, tn, tk = tile
-    return ws_gemm_config(tm, tn, tk, producer_waves, consumer_waves, stages, DTYPE_CODES[dtype])
+    return ws_gemm_config(tm, tn, tk, producer_waves, consumer_waves, stages, DTYPE_CODES[dtype],
+                          LOAD_PATHS[load_path])
 
 
 # -- C names -----------------------------------------------------------------
@@ -147,6 +154,10 @@ def ws_gemm_set_debug(h, dbg: ws_gemm_debug | None) -> int:
     return _lib.ws_gemm_set_debug(h, ctypes.byref(dbg) if dbg is not None else None)
 
 
+def ws_gemm_set_trace(h, buf_ptr: int | None, nbytes: int = 0, wgs: int = 0, iters: int = 0) -> int:
+    return _lib.ws_gemm_set_trace(h, _p(buf_ptr) if buf_ptr else None, nbytes, wgs, iters)
+
+
 def ws_gemm_destroy(h) -> int:
     return _lib.ws_gemm_destroy(h)
 
@@ -164,10 +175,10 @@ class WsGemm:
     """A created plan for one (M, N, K, configuration); call it on torch tensors."""
 
     def __init__(self, M, N, K, tile=(128, 128, 32), stages=3, producer_waves=4,
-                 consumer_waves=4, dtype="bf16"):
+                 consumer_waves=4, dtype="bf16", load_path="registers"):
         self.M, self.N, self.K = M, N, K
         self.dtype = dtype
-        self.cfg = config(tile, stages, producer_waves, consumer_waves, dtype)
+        self.cfg = config(tile, stages, producer_waves, consumer_waves, dtype, load_path)
         s, self._h = ws_gemm_create(M, N, K, self.cfg)
         if s != WS_OK:
             self._h = None

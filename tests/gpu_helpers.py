@@ -16,12 +16,13 @@ def log(msg: str) -> None:
     print(msg, flush=True)
 
 
-def run_gpu(A_cpu, B_cpu, tile, stages, np_, nc, dtype, C_fill=float("nan"), repeats=1):
+def run_gpu(A_cpu, B_cpu, tile, stages, np_, nc, dtype, C_fill=float("nan"), repeats=1,
+            load_path="registers"):
     """C = A B through the library on cuda:0; returns the last C as float32 numpy."""
     from paper_2506_11209_amd import wsgemm as w
     M, K = A_cpu.shape
     N = B_cpu.shape[1]
-    g = w.WsGemm(M, N, K, tile, stages, np_, nc, dtype)
+    g = w.WsGemm(M, N, K, tile, stages, np_, nc, dtype, load_path)
     try:
         A = A_cpu.cuda()
         B = B_cpu.cuda()

@@ -46,26 +46,28 @@ for dt in ("bf16", "f16"):
                 FAMILIES.append(((tm, tn, tk), 4, split, dt))
 
 
+@pytest.mark.parametrize("load_path", ["registers", "dma"])
 @pytest.mark.parametrize("tile,nc,split,dtype", FAMILIES,
                          ids=lambda x: "x".join(map(str, x)) if isinstance(x, tuple) else str(x))
-def test_family_exact_on_integers(tile, nc, split, dtype):
+def test_family_exact_on_integers(tile, nc, split, dtype, load_path):
     tm, tn, tk = tile
     M, N, K = 3 * tm, 5 * tn, 7 * tk  # 15 tiles, S = 7
     stages = 2 if fits(tile, 3) is False else 3
     A, B = inputs.make_operands(M, N, K, dtype, "int4", 100 + tm + tn + tk)
-    log("case family tile=%s nc=%d split=%d %s" % (tile, nc, split, dtype))
-    C = run_gpu(A, B, tile, stages, nc * split, nc, dtype)
+    log("case family tile=%s nc=%d split=%d %s %s" % (tile, nc, split, dtype, load_path))
+    C = run_gpu(A, B, tile, stages, nc * split, nc, dtype, load_path=load_path)
     r = check_full(C, A, B, dtype, exact=True)
     assert r["ok"], r
 
 
+@pytest.mark.parametrize("load_path", ["registers", "dma"])
 @pytest.mark.parametrize("stages", [2, 3, 4])
 @pytest.mark.parametrize("K", [64, 128, 192, 256])  # S = 1, 2, 3, 4 around the ring depth
-def test_ring_depth_edges(stages, K):
+def test_ring_depth_edges(stages, K, load_path):
     tile = (128, 128, 64)
     A, B = inputs.make_operands(256, 512, K, "bf16", "int4", 7 + K)
-    log("case ring stages=%d K=%d" % (stages, K))
-    C = run_gpu(A, B, tile, stages, 4, 4, "bf16")
+    log("case ring stages=%d K=%d %s" % (stages, K, load_path))
+    C = run_gpu(A, B, tile, stages, 4, 4, "bf16", load_path=load_path)
     assert check_full(C, A, B, "bf16", exact=True)["ok"]
 
 
@@ -108,12 +110,13 @@ def test_output_overwritten_and_deterministic():
 # (the paper's fast / slow DMA scenarios); a tiny poll limit forces the
 # watchdog, and every wave still exits.
 # ---------------------------------------------------------------------------
+@pytest.mark.parametrize("load_path", ["registers", "dma"])
 @pytest.mark.parametrize("pdelay,cdelay", [(3, 0), (0, 3)])
-def test_delays_keep_results_exact(pdelay, cdelay):
+def test_delays_keep_results_exact(pdelay, cdelay, load_path):
     from paper_2506_11209_amd import wsgemm as w
     A, B = inputs.make_operands(512, 512, 1024, "bf16", "int4", 9)
-    log("case delays p=%d c=%d" % (pdelay, cdelay))
-    g = w.WsGemm(512, 512, 1024, (128, 128, 64), 2, 4, 4, "bf16")
+    log("case delays p=%d c=%d %s" % (pdelay, cdelay, load_path))
+    g = w.WsGemm(512, 512, 1024, (128, 128, 64), 2, 4, 4, "bf16", load_path)
     try:
         g.set_debug(0, pdelay, cdelay)
         C = g(A.cuda(), B.cuda())
@@ -123,11 +126,12 @@ def test_delays_keep_results_exact(pdelay, cdelay):
         g.close()
 
 
-def test_watchdog_reports_timeout_then_recovers():
+@pytest.mark.parametrize("load_path", ["registers", "dma"])
+def test_watchdog_reports_timeout_then_recovers(load_path):
     from paper_2506_11209_amd import wsgemm as w
     A, B = inputs.make_operands(512, 512, 1024, "bf16", "int4", 10)
-    log("case watchdog")
-    g = w.WsGemm(512, 512, 1024, (128, 128, 64), 2, 4, 4, "bf16")
+    log("case watchdog %s" % load_path)
+    g = w.WsGemm(512, 512, 1024, (128, 128, 64), 2, 4, 4, "bf16", load_path)
     try:
         Ad, Bd = A.cuda(), B.cuda()
         g.set_debug(1, 20, 0)  # one poll allowed, producers ~160k cycles late
@@ -183,25 +187,27 @@ def full(name):
     return _cache[name]
 
 
-FULL_CASES = [(name, pt) for name in ("gemm_4096x4096x4096_bf16_normal",
-                                      "gemm_8192x8192x8192_bf16_normal",
-                                      "gemm_16384x256x8192_bf16_uniform",
-                                      "gemm_2048x2048x32768_bf16_normal_k")
-              for pt in WORKLOADS[name].points]
+FULL_CASES = [(name, pt, lp) for name in ("gemm_4096x4096x4096_bf16_normal",
+                                          "gemm_8192x8192x8192_bf16_normal",
+                                          "gemm_16384x256x8192_bf16_uniform",
+                                          "gemm_2048x2048x32768_bf16_normal_k")
+              for pt in WORKLOADS[name].points for lp in ("registers", "dma")]
 
 
-@pytest.mark.parametrize("name,point", FULL_CASES, ids=lambda x: "x".join(map(str, x)) if isinstance(x, tuple) else x)
-def test_full_size_workload(name, point):
+@pytest.mark.parametrize("name,point,load_path", FULL_CASES,
+                         ids=lambda x: "x".join(map(str, x)) if isinstance(x, tuple) else x)
+def test_full_size_workload(name, point, load_path):
     from paper_2506_11209_amd import wsgemm as w
     tm, tn, tk, stages, np_, nc = point
     f = full(name)
     wl = f.wl
-    log("case full %s point=%s" % (name, point))
+    log("case full %s point=%s %s" % (name, point, load_path))
     if not fits((tm, tn, tk), stages):
-        s, _ = w.ws_gemm_create(wl.M, wl.N, wl.K, w.config((tm, tn, tk), stages, np_, nc, wl.dtype))
+        s, _ = w.ws_gemm_create(wl.M, wl.N, wl.K, w.config((tm, tn, tk), stages, np_, nc, wl.dtype,
+                                                           load_path))
         assert s == w.WS_ERR_LDS_OVERFLOW
         return
-    g = w.WsGemm(wl.M, wl.N, wl.K, (tm, tn, tk), stages, np_, nc, wl.dtype)
+    g = w.WsGemm(wl.M, wl.N, wl.K, (tm, tn, tk), stages, np_, nc, wl.dtype, load_path)
     try:
         C = torch.full((wl.M, wl.N), float("nan"), dtype=torch.float32, device="cuda")
         g(f.Ad, f.Bd, C)
@@ -214,3 +220,24 @@ def test_full_size_workload(name, point):
     assert r["ok"], r
     ok, worst = freivalds(Ch, f.A64, f.B64, f.absA, f.absB)
     assert ok, worst
+
+
+# ---------------------------------------------------------------------------
+# Event trace: results stay exact, and per K-iteration the stamps are ordered
+# as the protocol requires (issue <= landed <= observed full <= release).
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("point", [(128, 128, 64, 3, 4, 4), (128, 128, 32, 4, 8, 4)])
+def test_trace_is_ordered_and_harmless(point):
+    from paper_2506_11209_amd.trace import rel, run_traced
+    from paper_2506_11209_amd.workloads import Workload
+    wl = Workload("trace_case", 1024, 1024, 1024, "bf16", "int4", 31, True)
+    A, B = inputs.make_operands(wl.M, wl.N, wl.K, wl.dtype, wl.dist, wl.seed)
+    rec, plan, C = run_traced(wl, point, wgs=2, Ad=A.cuda(), Bd=B.cuda())
+    assert check_full(C.cpu().numpy(), A, B, "bf16", exact=True)["ok"]
+    n = plan["iters"] * len(range(0, plan["tiles"], plan["grid"]))
+    t = rel(rec[0], n)
+    ia, ib, la, lb, ready, mma, relz = (t[:, i] for i in range(7))
+    assert np.all(la >= ia) and np.all(lb >= ib)
+    assert np.all(ready >= np.maximum(la, lb))
+    assert np.all(relz >= ready)
+    assert np.all(np.diff(mma) > 0)
