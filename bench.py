@@ -6,7 +6,7 @@ M = N = K = 8192, bf16 operands ~ N(0,1), fp32 output.  One step is one full
 C = A B.  Operands are generated once (seeded, synthetic) and are resident in
 HBM before the timed region starts.
 
-    python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--point TMxTNxTKxSxNPxNC]
+    python bench.py [--gpus 1] [--steps 100] [--warmup 50] [--point TMxTNxTKxSxNPxNC]
 
 Prints one JSON line.  Also reported: the dominant kernel's roofline entry
 (device time per launch from HIP events on the launch stream) and the CPU
@@ -24,10 +24,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 WORKLOAD = "gemm_8192x8192x8192_bf16_normal"
-DEFAULT_POINT = (128, 256, 64, 3, 4, 4)   # (TM, TN, TK, stages, producer waves, consumer waves)
-DEFAULT_LOAD_PATH = "registers"
+DEFAULT_POINT = (256, 128, 64, 3, 4, 4)   # (TM, TN, TK, stages, producer waves, consumer waves)
+DEFAULT_LOAD_PATH = "dma"
 PEAK_TFLOPS = 2500.0                      # MI355X dense bf16 MFMA
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+PROFILES = os.path.join(ROOT, "profiles")
 
 
 def kernel_fingerprint() -> str:
@@ -41,16 +41,20 @@ def kernel_fingerprint() -> str:
 
 
 def traffic_for(point_key: str):
-    """HBM bytes per launch from the committed counter runs, if they were
-    taken on the current kernel sources and this launch point."""
-    try:
-        with open(TRAFFIC_FILE) as f:
-            t = json.load(f)
-    except (OSError, ValueError):
-        return None
-    if t.get("kernel_fingerprint") != kernel_fingerprint() or t.get("point") != point_key:
-        return None
-    return t.get("traffic_bytes_per_launch")
+    """HBM bytes per launch from the committed counter runs (profiles/
+    *hbm_traffic*.json), if they were taken on the current kernel sources
+    and this launch point; else None."""
+    import glob
+    fp = kernel_fingerprint()
+    for path in sorted(glob.glob(os.path.join(PROFILES, "*hbm_traffic*.json"))):
+        try:
+            with open(path) as f:
+                t = json.load(f)
+        except (OSError, ValueError):
+            continue
+        if t.get("kernel_fingerprint") == fp and t.get("point") == point_key:
+            return t.get("traffic_bytes_per_launch")
+    return None
 
 
 def cpu_baseline(wl, target_s: float = 10.0):
@@ -79,8 +83,8 @@ def cpu_baseline(wl, target_s: float = 10.0):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--point", default=None, help="TMxTNxTKxSTAGESxNPxNC")
     ap.add_argument("--load-path", default=DEFAULT_LOAD_PATH, choices=("registers", "dma"))
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -1,0 +1,98 @@
+"""Summaries of rocprofv3 result databases (rocpd SQLite) as short text.
+
+    python -m paper_2506_11209_amd.profsummary trace  DB [--kernel SUBSTR] [--skip N]
+    python -m paper_2506_11209_amd.profsummary counters DB [--kernel SUBSTR]
+    python -m paper_2506_11209_amd.profsummary traffic FETCH_DB WRITE_DB CAL_FETCH_DB CAL_WRITE_DB \
+        --kernel SUBSTR --point KEY [--copy-mib 1024]
+
+`trace`: per-kernel call count, mean / median / min duration (us), from
+`rocprofv3 --kernel-trace`.  `counters`: per-kernel mean of each collected
+counter over its dispatches (instances summed per dispatch), from
+`rocprofv3 --pmc ...`.  `traffic`: HBM bytes per launch of a kernel from
+FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by bytes-moved /
+counter-reading of the known-size copy run by
+`python -m paper_2506_11209_amd.hbm_calibrate`; printed as the JSON record
+bench.py reads (tagged with the kernel-source fingerprint).
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import sqlite3
+import statistics
+
+
+def kernel_durations(db_path: str, kernel: str | None = None, skip: int = 0):
+    """Durations (us) per kernel name in dispatch order, the first `skip`
+    dispatches of each kernel (the untimed warm-up launches) left out."""
+    db = sqlite3.connect(db_path)
+    rows = db.execute("select name, duration from kernels order by start").fetchall()
+    out = collections.defaultdict(list)
+    for name, dur in rows:
+        if kernel is None or kernel in name:
+            out[name].append(dur / 1e3)  # ns -> us
+    return {k: v[skip:] for k, v in out.items() if len(v) > skip}
+
+
+def counter_means(db_path: str, kernel: str | None = None):
+    db = sqlite3.connect(db_path)
+    rows = db.execute("select name, dispatch_id, counter_name, counter_value from pmc_events").fetchall()
+    per = collections.defaultdict(float)
+    for name, did, cn, cv in rows:
+        if kernel is None or kernel in name:
+            per[(name, did, cn)] += cv
+    agg = collections.defaultdict(list)
+    for (name, did, cn), v in per.items():
+        agg[(name, cn)].append(v)
+    return {k: (statistics.fmean(v), len(v)) for k, v in agg.items()}
+
+
+def _mean_counter(db_path, name_part, counter):
+    vals = [v for (n, cn), (v, _) in counter_means(db_path).items() if name_part in n and cn == counter]
+    if not vals:
+        raise SystemExit("no %s for %s in %s" % (counter, name_part, db_path))
+    return vals[0]
+
+
+def traffic(fetch_db, write_db, cal_fetch_db, cal_write_db, kernel, point, copy_mib):
+    import json
+    import os
+    import sys
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    from bench import kernel_fingerprint
+    copy_bytes = copy_mib * (1 << 20)
+    f_scale = copy_bytes / (_mean_counter(cal_fetch_db, "copyBuffer", "FETCH_SIZE") * 1024)
+    w_scale = copy_bytes / (_mean_counter(cal_write_db, "copyBuffer", "WRITE_SIZE") * 1024)
+    fetch = _mean_counter(fetch_db, kernel, "FETCH_SIZE")
+    write = _mean_counter(write_db, kernel, "WRITE_SIZE")
+    rec = {"kernel": kernel, "point": point, "kernel_fingerprint": kernel_fingerprint(),
+           "fetch_size_kib": fetch, "write_size_kib": write,
+           "fetch_scale_bytes_per_kib": f_scale * 1024, "write_scale_bytes_per_kib": w_scale * 1024,
+           "traffic_bytes_per_launch": fetch * 1024 * f_scale + write * 1024 * w_scale}
+    print(json.dumps(rec, indent=1))
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("mode", choices=("trace", "counters", "traffic"))
+    ap.add_argument("db", nargs="+")
+    ap.add_argument("--kernel", default=None)
+    ap.add_argument("--point", default=None)
+    ap.add_argument("--copy-mib", type=int, default=1024)
+    ap.add_argument("--skip", type=int, default=0, help="trace: leading dispatches per kernel to drop")
+    a = ap.parse_args(argv)
+    if a.mode == "traffic":
+        traffic(*a.db[:4], a.kernel, a.point, a.copy_mib)
+        return
+    a.db = a.db[0]
+    if a.mode == "trace":
+        for name, d in sorted(kernel_durations(a.db, a.kernel, a.skip).items(), key=lambda x: -sum(x[1])):
+            print("%-72s calls=%-5d mean_us=%.2f median_us=%.2f min_us=%.2f" % (
+                name[:72], len(d), statistics.fmean(d), statistics.median(d), min(d)))
+    else:
+        for (name, cn), (mean, n) in sorted(counter_means(a.db, a.kernel).items()):
+            print("%-72s %-32s mean=%.6g dispatches=%d" % (name[:72], cn, mean, n))
+
+
+if __name__ == "__main__":
+    main()
