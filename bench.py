@@ -25,7 +25,7 @@ sys.path.insert(0, ROOT)
 
 WORKLOAD = "gemm_8192x8192x8192_bf16_normal"
 DEFAULT_POINT = (256, 128, 64, 3, 4, 4)   # (TM, TN, TK, stages, producer waves, consumer waves)
-DEFAULT_LOAD_PATH = "dma"
+DEFAULT_LOAD_PATH = "registers"
 PEAK_TFLOPS = 2500.0                      # MI355X dense bf16 MFMA
 PROFILES = os.path.join(ROOT, "profiles")
 

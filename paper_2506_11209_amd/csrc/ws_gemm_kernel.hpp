@@ -163,6 +163,30 @@ __device__ __forceinline__ void lds_signal(WSG_LDS uint32_t* p) {
 #endif
 }
 
+// signal() when `enable` (wave-uniform) is non-zero, as one asm block, so
+// the caller's control flow gets no join.
+template <int YOUNGER = 0>
+__device__ __forceinline__ void lds_signal_if(WSG_LDS uint32_t* p, uint32_t enable) {
+  static_assert(YOUNGER >= 0 && YOUNGER <= 15, "lgkmcnt range");
+#if defined(__HIP_DEVICE_COMPILE__)
+  const uint32_t addr = (uint32_t)(uintptr_t)p;
+  const uint32_t one = 1u;
+  uint64_t saved;
+  asm volatile(
+      "s_cmp_eq_u32 %4, 0\n\t"
+      "s_cbranch_scc1 1f\n\t"
+      "s_waitcnt lgkmcnt(%3)\n\t"
+      "s_mov_b64 %0, exec\n\t"
+      "s_mov_b64 exec, 1\n\t"
+      "ds_add_u32 %1, %2\n\t"
+      "s_mov_b64 exec, %0\n"
+      "1:"
+      : "=&s"(saved)
+      : "v"(addr), "v"(one), "n"(YOUNGER), "s"(__builtin_amdgcn_readfirstlane(enable))
+      : "memory", "scc");
+#endif
+}
+
 // Blocking read of an LDS counter, issued from asm so that the compiler does
 // not order it behind outstanding LDS-DMA loads (it cannot prove the counter
 // and the DMA destination are disjoint).  Result is wave-uniform.
@@ -236,8 +260,80 @@ __device__ __forceinline__ bool wait_counter(WSG_LDS uint32_t* ctr, uint32_t tar
   return status == 0;
 }
 
+// The same wait as one asm block, so that it adds no join to the caller's
+// control flow (the consumer's K loop stays a single basic block and its
+// operand registers are not shuffled around a join).  `seen` is a value of
+// *ctr read earlier: when it already satisfies the target, nothing is read.
+// Returns 0 when the counter reached the target, 1 when the workgroup abort
+// flag is up, 2 after `limit` polls; wave-uniform.
+__device__ __forceinline__ uint32_t wait_until(uint32_t seen, WSG_LDS uint32_t* ctr,
+                                               WSG_LDS uint32_t* abort_flag, uint32_t target,
+                                               int32_t limit, uint32_t enable = 1) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const uint32_t ca = (uint32_t)(uintptr_t)ctr, aa = (uint32_t)(uintptr_t)abort_flag;
+  uint32_t st, spins, v0, v1;
+  asm volatile(
+      "s_mov_b32 %[st], 0\n\t"
+      "s_cmp_eq_u32 %[en], 0\n\t"
+      "s_cbranch_scc1 2f\n\t"
+      "v_readfirstlane_b32 %[st], %[seen]\n\t"
+      "s_sub_u32 %[st], %[st], %[target]\n\t"
+      "s_cmp_ge_i32 %[st], 0\n\t"
+      "s_mov_b32 %[st], 0\n\t"
+      "s_cbranch_scc1 2f\n\t"
+      "s_mov_b32 %[spins], 0\n"
+      "1:\n\t"
+      "ds_read_b32 %[v0], %[ca]\n\t"
+      "ds_read_b32 %[v1], %[aa]\n\t"
+      "s_waitcnt lgkmcnt(0)\n\t"
+      "v_readfirstlane_b32 %[st], %[v0]\n\t"
+      "s_sub_u32 %[st], %[st], %[target]\n\t"
+      "s_cmp_ge_i32 %[st], 0\n\t"
+      "s_mov_b32 %[st], 0\n\t"
+      "s_cbranch_scc1 2f\n\t"
+      "v_readfirstlane_b32 %[st], %[v1]\n\t"
+      "s_cmp_lg_u32 %[st], 0\n\t"
+      "s_mov_b32 %[st], 1\n\t"
+      "s_cbranch_scc1 2f\n\t"
+      "s_add_u32 %[spins], %[spins], 1\n\t"
+      "s_cmp_gt_i32 %[spins], %[limit]\n\t"
+      "s_mov_b32 %[st], 2\n\t"
+      "s_cbranch_scc1 2f\n\t"
+      "s_sleep 1\n\t"
+      "s_branch 1b\n"
+      "2:"
+      : [st] "=&s"(st), [spins] "=&s"(spins), [v0] "=&v"(v0), [v1] "=&v"(v1)
+      : [seen] "v"(seen), [target] "s"(__builtin_amdgcn_readfirstlane(target)), [ca] "v"(ca),
+        [aa] "v"(aa), [limit] "s"(limit), [en] "s"(__builtin_amdgcn_readfirstlane(enable))
+      : "memory", "scc");
+  return st;
+#else
+  if (!enable) return 0u;
+  return (int32_t)(*ctr - target) >= 0 ? 0u : (*abort_flag ? 1u : 2u);
+#endif
+}
+
+// Test hook: n bursts of ~8k-cycle sleeps (n wave-uniform; 0 in production),
+// as one asm block so that the caller's loop gets no join.
 __device__ __forceinline__ void debug_delay(int n) {
-  for (int i = 0; i < n; ++i) __builtin_amdgcn_s_sleep(127);
+#if defined(__HIP_DEVICE_COMPILE__)
+  uint32_t left;
+  asm volatile(
+      "s_mov_b32 %0, %1\n\t"
+      "s_cmp_le_i32 %0, 0\n\t"
+      "s_cbranch_scc1 2f\n"
+      "1:\n\t"
+      "s_sleep 127\n\t"
+      "s_sub_u32 %0, %0, 1\n\t"
+      "s_cmp_lg_u32 %0, 0\n\t"
+      "s_cbranch_scc1 1b\n"
+      "2:"
+      : "=&s"(left)
+      : "s"(__builtin_amdgcn_readfirstlane(n))
+      : "scc");
+#else
+  (void)n;
+#endif
 }
 
 template <bool BF16>
@@ -384,7 +480,7 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
           }
         }
       }
-      if (args.producer_delay) debug_delay(args.producer_delay);
+      debug_delay(args.producer_delay);
       compiler_fence();
       if (tracing && a_rank == 0 && DO_A) lds_stamp(&full[kStampIssueA + slot], cycles32());
       WSG_LDS char* a_dst = smem + kHeaderBytes + slot * G::STAGE;
@@ -525,7 +621,7 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
           }
         }
       }
-      if (args.producer_delay) debug_delay(args.producer_delay);
+      debug_delay(args.producer_delay);
       compiler_fence();
       WSG_LDS char* base = smem + kHeaderBytes + slot * G::STAGE + lane16;
 #pragma unroll
@@ -580,42 +676,35 @@ __device__ __forceinline__ void producer(const KernelArgs& args, WSG_LDS char* s
 }
 
 // ---------------------------------------------------------------------------
-// Consumer (MATH wave).  Software-pipelined over MFMA k-steps: operands of
-// step s + 1 are read from LDS while the MFMAs of step s run.  The slot of a
-// K-iteration is released as soon as its last operands are in registers, and
-// the next slot's counter is peeked one k-step early so the wait costs no
-// latency when the producers are ahead.
+// Consumer (MATH wave).  One K-iteration is KS MFMA k-steps of 16.  Inside a
+// k-step the MFMAs run M-major: every column block nb of row block mb, then
+// the next row block.  Operands for k-step s + 1 are read while k-step s
+// multiplies:
+//   * the B fragments of k-step s + 1 go to the other of two buffers at the
+//     start of k-step s;
+//   * A fragment mb is single-buffered and refilled right after its row of
+//     MFMAs, (BM - 1) * BN MFMAs before its next use.
+// The last k-step of a K-iteration reads k-step 0 of the next slot: the slot's
+// full[] counter was peeked one k-step earlier, so the wait costs nothing
+// when the producers are ahead.  The slot is released (empty[] signal) right
+// after that k-step's reads are issued, once the older reads have completed.
 // ---------------------------------------------------------------------------
 template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16>
 struct ConsumerOps {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
   static constexpr int kReads = G::BM + 2 * G::BN;  // LDS reads per k-step
-  static constexpr int kMfma = G::BM * G::BN;       // MFMAs per k-step
-  // A operand of block mb at k-step s: 16 bytes at a_off[s] + mb * 32 rows.
-  // B operand of block nb at k-step s: two transposed 8-byte reads.
-  static __device__ __forceinline__ void load(i16x8_t (&fa)[G::BM], i16x8_t (&fb)[G::BN],
-                                              WSG_LDS char* a_src, WSG_LDS char* b_src,
-                                              uint32_t a_off, uint32_t b_off, int s) {
-#pragma unroll
-    for (int mb = 0; mb < G::BM; ++mb)
-      fa[mb] = *(WSG_LDS i16x8_t*)(a_src + a_off + mb * 32 * TK * 2);
-#pragma unroll
-    for (int nb = 0; nb < G::BN; ++nb) {
-      WSG_LDS char* p = b_src + b_off + ((4 * s) * G::NQ + 2 * nb) * 128;
-      const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((WSG_LDS i16x4_t*)p);
-      const i16x4_t hi =
-          __builtin_amdgcn_ds_read_tr16_b64_v4i16((WSG_LDS i16x4_t*)(p + G::NQ * 128));
-      fb[nb] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-    }
+  // A operand of row block mb: 16 bytes per lane at a_src + a_off + mb * 32 rows.
+  static __device__ __forceinline__ void load_a(i16x8_t& fa, WSG_LDS char* a_src, uint32_t a_off,
+                                                int mb) {
+    fa = *(WSG_LDS i16x8_t*)(a_src + a_off + mb * 32 * TK * 2);
   }
-  static __device__ __forceinline__ void mma(f32x16_t (&acc)[G::BM][G::BN],
-                                             const i16x8_t (&fa)[G::BM],
-                                             const i16x8_t (&fb)[G::BN]) {
-#pragma unroll
-    for (int mb = 0; mb < G::BM; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < G::BN; ++nb)
-        acc[mb][nb] = mfma32x32x16<BF16>(fa[mb], fb[nb], acc[mb][nb]);
+  // B operand of column block nb at k-step s: two transposed 8-byte reads.
+  static __device__ __forceinline__ void load_b(i16x8_t& fb, WSG_LDS char* b_src, uint32_t b_off,
+                                                int s, int nb) {
+    WSG_LDS char* p = b_src + b_off + ((4 * s) * G::NQ + 2 * nb) * 128;
+    const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((WSG_LDS i16x4_t*)p);
+    const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((WSG_LDS i16x4_t*)(p + G::NQ * 128));
+    fb = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   }
 };
 
@@ -624,12 +713,7 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
                                          int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
   using Ops = ConsumerOps<TM, TN, TK, NC, SPLIT, BF16>;
-  static_assert(G::KS % 2 == 0, "k-steps per K-iteration must be even");
-  // Operand prefetch distance in k-steps, and fragment buffers (buffer of
-  // k-step s is s % NB, the same in every K-iteration).
-  constexpr int D = (G::KS >= 4) ? 3 : 1;
-  constexpr int NB = (D == 1) ? 2 : G::KS;
-  static_assert(NB >= D + 1 && G::KS % NB == 0, "fragment buffers must cover the prefetch");
+  static_assert(G::KS >= 2, "a K-iteration holds at least two k-steps");
   WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
   WSG_LDS uint32_t* empty = full + kMaxStages;
   WSG_LDS uint32_t* abort_flag = full + 2 * kMaxStages;
@@ -668,9 +752,8 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
   for (int mb = 0; mb < G::BM; ++mb)
 #pragma unroll
     for (int nb = 0; nb < G::BN; ++nb) acc[mb][nb] = f32x16_t{};
-
-  i16x8_t fa[NB][G::BM];
-  i16x8_t fb[NB][G::BN];
+  i16x8_t fa[G::BM];
+  i16x8_t fb[2][G::BN];
 
   // Event trace (consumer wave 0 of traced workgroups writes the records).
   const bool tracing = TRACE && args.trace != nullptr && cw == 0 && (int)blockIdx.x < args.trace_wgs;
@@ -690,79 +773,66 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
     }
   };
 
-  // Prologue: wait for K-iteration 0 and read its first D k-steps.
+  // Prologue: wait for K-iteration 0 and read k-step 0.
   if (!wait_counter(&full[0], (uint32_t)G::NP, abort_flag, args.spin_limit, args.err)) return;
   record_ready(0, 0);
 #pragma unroll
-  for (int s = 0; s < D; ++s)
-    Ops::load(fa[s], fb[s], smem + kHeaderBytes, smem + kHeaderBytes + G::A_BYTES, a_off[s],
-              b_off, s);
+  for (int mb = 0; mb < G::BM; ++mb) Ops::load_a(fa[mb], smem + kHeaderBytes, a_off[0], mb);
+#pragma unroll
+  for (int nb = 0; nb < G::BN; ++nb)
+    Ops::load_b(fb[0][nb], smem + kHeaderBytes + G::A_BYTES, b_off, 0, nb);
 
-  constexpr int RA = G::KS - D;  // region that acquires the next slot
-  constexpr int RR = RA + 1;      // region that releases the current slot
-  static_assert(RA >= 1, "the next slot is peeked one region before it is acquired");
-  uint32_t rel_slot = 0;
-  bool rel_pending = false;
   uint32_t q = 0, kk = 0;
   while (true) {
     const uint32_t slot = q % P;
     WSG_LDS char* a_src = smem + kHeaderBytes + slot * G::STAGE;
     WSG_LDS char* b_src = a_src + G::A_BYTES;
     const bool has_next = (q + 1) < total;
+    // After the last K-iteration the next-slot reads re-read this slot (and
+    // are never used), so every path issues the same LDS operations.
     const uint32_t nslot = has_next ? (q + 1) % P : slot;
-    const uint32_t ntarget = ((q + 1) / P + 1) * (uint32_t)G::NP;
+    const uint32_t ntarget = has_next ? ((q + 1) / P + 1) * (uint32_t)G::NP : 0u;
     WSG_LDS char* na_src = smem + kHeaderBytes + nslot * G::STAGE;
     WSG_LDS char* nb_src = na_src + G::A_BYTES;
     uint32_t peek = 0;
-    if (args.consumer_delay) debug_delay(args.consumer_delay);
+    debug_delay(args.consumer_delay);
     if (tracing) record(q, 5, cycles32());
-
-    // Region s: read the operands of k-step s + D, multiply k-step s.
-    //   region RA = KS - D: wait() for slot q+1 (peeked one region earlier,
-    //     before that region's reads), then read its first k-step;
-    //   region RR = RA + 1: signal() slot q free, waiting only for the reads
-    //     older than region RA's (RR == KS: region 0 of the next K-iteration).
 #pragma unroll
     for (int s = 0; s < G::KS; ++s) {
-      const int tp = s + D;
-      if (RR == G::KS && s == 0 && rel_pending) {
-        lds_signal<Ops::kReads>(&empty[rel_slot]);
-        if (tracing) record(q - 1, 6, cycles32());
-        rel_pending = false;
+      const int cur = s & 1, nxt = cur ^ 1;
+      const bool last = (s == G::KS - 1);
+      if (s == G::KS - 2) {
+        peek = lds_peek(&full[nslot]);  // before this k-step's reads
+        __builtin_amdgcn_sched_barrier(0);
       }
-      if (RR < G::KS && s == RR) {
-        lds_signal<Ops::kReads>(&empty[slot]);
-        if (tracing) record(q, 6, cycles32());
-      }
-      if (s == RA) {
-        if (has_next && (int32_t)(__builtin_amdgcn_readfirstlane(peek) - ntarget) < 0) {
-          if (!wait_counter(&full[nslot], ntarget, abort_flag, args.spin_limit, args.err)) return;
+      if (last) {
+        const uint32_t st = wait_until(peek, &full[nslot], abort_flag, ntarget, args.spin_limit);
+        if (st != 0) {
+          if (st == 2) report_timeout(abort_flag, args.err);
+          return;
         }
         compiler_fence();
         if (tracing && has_next) record_ready(q + 1, nslot);
       }
-      if (s == RA - 1) {
-        peek = lds_peek(&full[nslot]);
+      WSG_LDS char* ra = last ? na_src : a_src;
+      WSG_LDS char* rb = last ? nb_src : b_src;
+      const int ts = last ? 0 : s + 1;
+#pragma unroll
+      for (int nb = 0; nb < G::BN; ++nb) Ops::load_b(fb[nxt][nb], rb, b_off, ts, nb);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int mb = 0; mb < G::BM; ++mb) {
+#pragma unroll
+        for (int nb = 0; nb < G::BN; ++nb)
+          acc[mb][nb] = mfma32x32x16<BF16>(fa[mb], fb[cur][nb], acc[mb][nb]);
+        Ops::load_a(fa[mb], ra, a_off[ts], mb);
         __builtin_amdgcn_sched_barrier(0);
       }
-      if (tp < G::KS) {
-        Ops::load(fa[tp % NB], fb[tp % NB], a_src, b_src, a_off[tp], b_off, tp);
-        Ops::mma(acc, fa[s % NB], fb[s % NB]);
-        __builtin_amdgcn_sched_group_barrier(0x100, Ops::kReads, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, Ops::kMfma, 0);
-      } else {
-        // Unconditional, so the compiler's LDS wait counts stay exact on
-        // every path; after the last K-iteration these re-read the current
-        // slot and are never used.
-        Ops::load(fa[(tp - G::KS) % NB], fb[(tp - G::KS) % NB], na_src, nb_src,
-                  a_off[tp - G::KS], b_off, tp - G::KS);
-        Ops::mma(acc, fa[s % NB], fb[s % NB]);
+      if (last) {
+        // Every read of this slot is older than the kReads just issued.
+        lds_signal<Ops::kReads>(&empty[slot]);
+        if (tracing) record(q, 6, cycles32());
       }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if (RR == G::KS) {
-      rel_slot = slot;
-      rel_pending = true;
     }
     ++q;
     if (++kk == S) {
@@ -785,13 +855,168 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
             *(float*)(rowp + lane_off + nb * 128) = acc[mb][nb][e];
         }
       if (tracing) record(q - 1, 7, cycles32());
-      if (!has_next) {
-        if (RR == G::KS && rel_pending) {  // every slot use is released, the last one too
-          lds_signal<0>(&empty[rel_slot]);
-          if (tracing) record(q - 1, 6, cycles32());
-        }
-        break;
+      if (!has_next) break;
+      kk = 0;
+      v += Gd;
+      tile_coords(v, args.tiles_m, args.tiles_n, args.group_m, &ti, &tj);
+#pragma unroll
+      for (int mb = 0; mb < G::BM; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < G::BN; ++nb) acc[mb][nb] = f32x16_t{};
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Register-lean consumer for three waves per SIMD (two producers per consumer
+// with the largest wave tiles): every operand fragment is single-buffered and
+// refilled right after its last MFMA of the k-step, and the loop body is one
+// k-step, so each fragment has a single load site and keeps its registers.
+// Waits and releases are branch-free asm blocks enabled on the last k-step
+// of a K-iteration.  Same synchronisation as consumer().
+// ---------------------------------------------------------------------------
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE>
+__device__ __forceinline__ void consumer_rolling(const KernelArgs& args, WSG_LDS char* smem, int cw,
+                                                 int lane) {
+  using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
+  using Ops = ConsumerOps<TM, TN, TK, NC, SPLIT, BF16>;
+  WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
+  WSG_LDS uint32_t* empty = full + kMaxStages;
+  WSG_LDS uint32_t* abort_flag = full + 2 * kMaxStages;
+
+  const int wm = cw / G::WGN, wn = cw % G::WGN;
+  // A operand of k-step s: a_off0 ^ (32 s).  The chunk of k-step s is
+  // (2 s + lane / 32) ^ swz, and XOR acts bit by bit, so only bits 5.. of the
+  // in-row byte offset change with s.
+  const int r = wm * G::WM + (lane & 31);
+  const uint32_t a_off0 = (uint32_t)(r * TK * 2 + (((lane >> 5) ^ swz_a<TK>(r)) << 4));
+  const int grp = lane >> 4;
+  const uint32_t b_off =
+      (uint32_t)(((2 * (grp >> 1)) * G::NQ + (wn * G::WN) / 16 + (grp & 1)) * 128 + 8 * (lane & 15));
+  const uint32_t ring = (uint32_t)(uintptr_t)smem + kHeaderBytes;
+
+  const int Gd = gridDim.x;
+  const int g0 = first_slot(args);
+  if (g0 >= args.num_tiles) return;
+  const int my_tiles = (args.num_tiles - g0 + Gd - 1) / Gd;
+  const uint32_t S = (uint32_t)args.iters;
+  const uint32_t total = (uint32_t)my_tiles * S;
+  const uint32_t P = (uint32_t)args.stages;
+  const int N = args.N;
+
+  int v = g0;
+  int ti, tj;
+  tile_coords(v, args.tiles_m, args.tiles_n, args.group_m, &ti, &tj);
+
+  f32x16_t acc[G::BM][G::BN];
+#pragma unroll
+  for (int mb = 0; mb < G::BM; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < G::BN; ++nb) acc[mb][nb] = f32x16_t{};
+  i16x8_t fa[G::BM];
+  i16x8_t fb[G::BN];
+
+  const bool tracing = TRACE && args.trace != nullptr && cw == 0 && (int)blockIdx.x < args.trace_wgs;
+  uint32_t* trec = tracing ? args.trace + (size_t)blockIdx.x * args.trace_iters * kTraceEvents : nullptr;
+  auto record = [&](uint32_t iq, int ev, uint32_t value) {
+    if (tracing && iq < (uint32_t)args.trace_iters && lane == 0) trec[iq * kTraceEvents + ev] = value;
+  };
+  auto record_ready = [&](uint32_t iq, uint32_t ps) {
+    if (tracing) {
+      const uint32_t t = cycles32();
+      record(iq, 0, lds_read_now(&full[kStampIssueA + ps]));
+      record(iq, 1, lds_read_now(&full[kStampIssueB + ps]));
+      record(iq, 2, lds_read_now(&full[kStampLandA + ps]));
+      record(iq, 3, lds_read_now(&full[kStampLandB + ps]));
+      record(iq, 4, t);
+    }
+  };
+
+  if (!wait_counter(&full[0], (uint32_t)G::NP, abort_flag, args.spin_limit, args.err)) return;
+  record_ready(0, 0);
+  // full[] of the slot the next wait is for, read one k-step before that
+  // wait.  Read here before the first operand loads, so that on every path
+  // into the loop a whole k-step of loads is younger than it and the wait
+  // for it does not drain them.
+  uint32_t peek = lds_peek(&full[1 % P]);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int mb = 0; mb < G::BM; ++mb) Ops::load_a(fa[mb], smem + kHeaderBytes, a_off0, mb);
+#pragma unroll
+  for (int nb = 0; nb < G::BN; ++nb)
+    Ops::load_b(fb[nb], smem + kHeaderBytes + G::A_BYTES, b_off, 0, nb);
+
+  uint32_t q = 0, kk = 0, s = 0;
+  uint32_t slot = 0, nslot = 1 % P;
+  // full[nslot] reaches ntarget once K-iteration q + 1 has landed: that is
+  // slot use (q + 1) / P, and every producer signals once per use.
+  uint32_t ntarget = (1u / P + 1u) * (uint32_t)G::NP;
+  while (true) {
+    const uint32_t last = (s == (uint32_t)G::KS - 1) ? 1u : 0u;
+    const bool has_next = (q + 1) < total;
+    const uint32_t do_wait = (last && has_next) ? 1u : 0u;
+    debug_delay(s == 0 ? args.consumer_delay : 0);
+    if (tracing && s == 0) record(q, 5, cycles32());
+    const uint32_t st = wait_until(peek, &full[nslot], abort_flag, ntarget, args.spin_limit, do_wait);
+    if (st != 0) {
+      if (st == 2) report_timeout(abort_flag, args.err);
+      return;
+    }
+    compiler_fence();
+    if (tracing && do_wait) record_ready(q + 1, nslot);
+    {
+      const uint32_t pslot = last ? ((nslot + 1 == P) ? 0u : nslot + 1) : nslot;
+      peek = lds_peek(&full[pslot]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // Source of the next k-step: k-step s + 1 of this slot, or k-step 0 of
+    // the next slot (this slot again after the last K-iteration; never used).
+    const uint32_t ts = last ? 0u : s + 1;
+    const uint32_t src = ring + (do_wait ? nslot : slot) * (uint32_t)G::STAGE;
+    WSG_LDS char* ra = (WSG_LDS char*)(uintptr_t)(src);
+    WSG_LDS char* rb = (WSG_LDS char*)(uintptr_t)(src + G::A_BYTES + ts * (uint32_t)(4 * G::NQ * 128));
+    const uint32_t a_off = a_off0 ^ (32u * ts);
+#pragma unroll
+    for (int nb = 0; nb < G::BN; ++nb) {
+#pragma unroll
+      for (int mb = 0; mb < G::BM; ++mb) {
+        acc[mb][nb] = mfma32x32x16<BF16>(fa[mb], fb[nb], acc[mb][nb]);
+        if (nb == G::BN - 1) Ops::load_a(fa[mb], ra, a_off, mb);
+        __builtin_amdgcn_sched_barrier(0);
       }
+      Ops::load_b(fb[nb], rb, b_off, 0, nb);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // Every read of this slot is older than the kReads just issued.
+    lds_signal_if<Ops::kReads>(&empty[slot], last);
+    if (!last) {
+      ++s;
+      continue;
+    }
+    if (tracing) record(q, 6, cycles32());
+    s = 0;
+    slot = nslot;
+    nslot = (nslot + 1 == P) ? 0u : nslot + 1;
+    if (nslot == 0) ntarget += (uint32_t)G::NP;
+    ++q;
+    if (++kk == S) {
+      uint32_t ldc = (uint32_t)N * 4u;
+      asm volatile("" : "+s"(ldc));
+      char* cbase = (char*)args.C +
+                    (((int64_t)ti * TM + wm * G::WM) * (int64_t)N + (int64_t)tj * TN + wn * G::WN) * 4;
+      const uint32_t lane_off = (uint32_t)(4 * (lane >> 5)) * ldc + (uint32_t)(lane & 31) * 4u;
+#pragma unroll
+      for (int mb = 0; mb < G::BM; ++mb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          char* rowp = cbase + (uint32_t)(mb * 32 + 8 * (e >> 2) + (e & 3)) * ldc;
+#pragma unroll
+          for (int nb = 0; nb < G::BN; ++nb)
+            *(float*)(rowp + lane_off + nb * 128) = acc[mb][nb][e];
+        }
+      if (tracing) record(q - 1, 7, cycles32());
+      if (!has_next) break;
       kk = 0;
       v += Gd;
       tile_coords(v, args.tiles_m, args.tiles_n, args.group_m, &ti, &tj);
@@ -813,8 +1038,14 @@ __global__ void __launch_bounds__((NC + NC * SPLIT) * 64) ws_gemm_kernel(KernelA
   const int lane = threadIdx.x & 63;
   if (threadIdx.x < 2 * kMaxStages + 1) ((WSG_LDS uint32_t*)smem)[threadIdx.x] = 0u;
   __syncthreads();
-  if (wave < NC)
-    consumer<TM, TN, TK, NC, SPLIT, BF16, TRACE>(args, smem, wave, lane);
+  if (wave < NC) {
+    // Three waves per SIMD leave 168 VGPRs: the largest wave tiles then take
+    // the single-buffered consumer.
+    if constexpr (G::NW > 8 && G::BM * G::BN >= 8)
+      consumer_rolling<TM, TN, TK, NC, SPLIT, BF16, TRACE>(args, smem, wave, lane);
+    else
+      consumer<TM, TN, TK, NC, SPLIT, BF16, TRACE>(args, smem, wave, lane);
+  }
   else
     producer<TM, TN, TK, NC, SPLIT, BF16, TRACE>(args, smem, wave - NC, lane);
 }
