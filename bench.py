@@ -30,11 +30,16 @@ PEAK_TFLOPS = 2500.0                      # MI355X dense bf16 MFMA
 PROFILES = os.path.join(ROOT, "profiles")
 
 
+# Sources the GEMM kernel and its launch are built from (host-only model code
+# and the like do not change the kernel's memory traffic).
+KERNEL_SOURCES = ("ws_gemm_api.cpp", "ws_gemm_kernel.hpp", "ws_gemm_plan.hpp", "ws_gemm_registry.hpp")
+
+
 def kernel_fingerprint() -> str:
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2506_11209_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
+    for name in KERNEL_SOURCES:
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode() + f.read())
     return h.hexdigest()[:16]

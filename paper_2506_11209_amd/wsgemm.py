@@ -1,4 +1,5 @@
-"""ctypes binding of libwsgemm.so (declared in include/ws_gemm.h).
+"""ctypes binding of libwsgemm.so (declared in include/ws_gemm.h and
+include/ws_model.h).
 
 Functions carry the C names and only marshal arguments; every step of the
 GEMM runs in the library's HIP kernels.  Importing this module raises if the
@@ -60,6 +61,26 @@ class ws_gemm_debug(ctypes.Structure):
                 ("consumer_delay", ctypes.c_int32)]
 
 
+class ws_model_params(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in (
+        "t_init", "t_epilogue", "compute_throughput", "compute_latency", "load_throughput",
+        "load_latency")]
+
+
+class ws_model_options(ctypes.Structure):
+    _fields_ = [("two_dma", ctypes.c_int32), ("persistent", ctypes.c_int32),
+                ("finish_math", ctypes.c_int32)]
+
+
+class ws_model_result(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in (
+        "total_us", "round_us", "t_math", "t_load_a", "t_load_b", "wait_us")] + [
+        ("rounds", ctypes.c_int32), ("iters", ctypes.c_int32)]
+
+    def as_dict(self) -> dict:
+        return {n: getattr(self, n) for n, _ in self._fields_}
+
+
 _h = ctypes.c_void_p
 _p = ctypes.c_void_p
 _i64, _i32 = ctypes.c_int64, ctypes.c_int32
@@ -91,6 +112,14 @@ _lib.ws_gemm_set_trace.argtypes = [_h, _p, _i64, _i32, _i32]
 _lib.ws_gemm_set_trace.restype = _i32
 _lib.ws_gemm_destroy.argtypes = [_h]
 _lib.ws_gemm_destroy.restype = _i32
+_lib.ws_model_predict.argtypes = [_i64, _i64, _i64, _i32, _i32, _i32, _i32, _i32,
+                                  ctypes.POINTER(ws_model_params), ctypes.POINTER(ws_model_options),
+                                  ctypes.POINTER(ws_model_result)]
+_lib.ws_model_predict.restype = _i32
+_dp = ctypes.POINTER(ctypes.c_double)
+_lib.ws_model_events.argtypes = [_i32, _i32, _i32, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                 ctypes.c_double, ctypes.POINTER(ws_model_options), _dp, _dp, _dp]
+_lib.ws_model_events.restype = _i32
 
 
 def library() -> ctypes.CDLL:
@@ -232,3 +261,30 @@ class WsGemm:
             self.close()
         except Exception:
             pass
+
+
+# -- performance model (include/ws_model.h) ----------------------------------
+
+def model_options(two_dma=False, persistent=False, finish_math=False) -> ws_model_options:
+    return ws_model_options(int(two_dma), int(persistent), int(finish_math))
+
+
+def ws_model_predict(M, N, K, tile_m, tile_n, tile_k, stages, slots, params: ws_model_params,
+                     opts: ws_model_options | None = None):
+    r = ws_model_result()
+    s = _lib.ws_model_predict(M, N, K, tile_m, tile_n, tile_k, stages, slots, ctypes.byref(params),
+                              ctypes.byref(opts) if opts is not None else None, ctypes.byref(r))
+    return s, r
+
+
+def ws_model_events(iters, rounds, stages, t_math, t_load_a, t_load_b, t_epilogue,
+                    opts: ws_model_options | None = None):
+    """Returns (status, s_a, s_b, s_m) as lists; entry j is the paper's j + 1."""
+    persistent = opts is not None and opts.persistent
+    n = iters * rounds if persistent else iters
+    if n <= 0:
+        return WS_ERR_INVALID_ARG, [], [], []
+    arrs = [(ctypes.c_double * n)() for _ in range(3)]
+    s = _lib.ws_model_events(iters, rounds, stages, t_math, t_load_a, t_load_b, t_epilogue,
+                             ctypes.byref(opts) if opts is not None else None, *arrs)
+    return s, [list(a) for a in arrs][0], list(arrs[1]), list(arrs[2])
