@@ -40,7 +40,7 @@
 extern "C" {
 #endif
 
-#define WS_GEMM_ABI_VERSION 2
+#define WS_GEMM_ABI_VERSION 3
 
 typedef struct ws_gemm_handle* ws_gemm_t; /* opaque handle */
 
@@ -148,6 +148,38 @@ ws_status ws_gemm_set_debug(ws_gemm_t h, const ws_gemm_debug* dbg);
  * NULL buffer turns tracing off.  Tracing costs a few instructions per
  * K-iteration in the traced workgroups. */
 ws_status ws_gemm_set_trace(ws_gemm_t h, void* buffer, int64_t bytes, int32_t wgs, int32_t iters);
+
+/* Calibration kernels of the performance model (paper, Section 4.2, "Measure
+ * the Kernel Launch Time", "Measure the Epilogue Time", "Estimate the
+ * Throughput and Startup Latency of the DMA and MATH Warps").  Each is the
+ * GEMM kernel of cfg with one role reduced, launched with the GEMM's own
+ * plan (grid, block, LDS ring), so it measures that kernel's costs:
+ *   WS_CALIB_EMPTY     an empty kernel with the same launch (T_INIT);
+ *   WS_CALIB_LOAD_A    producers load only the A tiles of every K-iteration
+ *                      into the ring; consumers free each slot unread;
+ *   WS_CALIB_LOAD_B    the same with only the B tiles;
+ *   WS_CALIB_MATH      producers free slots without loading; consumers read
+ *                      and multiply whatever the slots hold (no C stores);
+ *   WS_CALIB_EPILOGUE  consumers store one zero tile per output tile, with
+ *                      no K loop (T_EPILOGUE); the producers exit;
+ *   WS_CALIB_LOAD_AB   producers load both tiles as in the GEMM; consumers
+ *                      free each slot unread (the producers' own rate).
+ * Run with ws_gemm_run (A, B, C as for the GEMM).  C is only written by
+ * WS_CALIB_EPILOGUE (zeros); the other kinds leave it untouched.  Tracing is
+ * not available on these handles.  WS_ERR_UNSUPPORTED when no calibration
+ * variant of cfg was compiled. */
+typedef enum {
+  WS_CALIB_NONE = -1, /* the GEMM itself (ws_gemm_create) */
+  WS_CALIB_EMPTY = 0,
+  WS_CALIB_LOAD_A = 1,
+  WS_CALIB_LOAD_B = 2,
+  WS_CALIB_MATH = 3,
+  WS_CALIB_EPILOGUE = 4,
+  WS_CALIB_LOAD_AB = 5
+} ws_calib_kind;
+
+ws_status ws_gemm_create_calibration(int64_t M, int64_t N, int64_t K, const ws_gemm_config* cfg,
+                                     int32_t kind, ws_gemm_t* out);
 
 /* Free the handle; NULL is a no-op.  Must not race with runs using it. */
 ws_status ws_gemm_destroy(ws_gemm_t h);

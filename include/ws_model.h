@@ -79,6 +79,15 @@ ws_status ws_model_predict(int64_t M, int64_t N, int64_t K, int32_t tile_m, int3
                            const ws_model_params* params, const ws_model_options* opts,
                            ws_model_result* out);
 
+/* The same prediction from explicit per-K-iteration costs (T_MATH, T_LOAD-A,
+ * T_LOAD-B measured for this configuration instead of the linear cost
+ * model); params->t_init and params->t_epilogue are used, the throughputs
+ * and latencies are ignored. */
+ws_status ws_model_predict_costs(int64_t M, int64_t N, int64_t K, int32_t tile_m, int32_t tile_n,
+                                 int32_t tile_k, int32_t stages, int32_t slots, double t_math,
+                                 double t_load_a, double t_load_b, const ws_model_params* params,
+                                 const ws_model_options* opts, ws_model_result* out);
+
 /* Event times of one workgroup.  Writes n = iters (per-round schedule) or
  * n = rounds x iters (persistent) entries to each caller-owned array;
  * entry j holds the paper's index j + 1.  Any of s_a, s_b, s_m may be NULL. */

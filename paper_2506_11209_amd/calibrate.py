@@ -1,0 +1,165 @@
+"""Calibrate the performance model on this GPU (paper, Section 4.2).
+
+    python -m paper_2506_11209_amd.calibrate [--load-paths registers,dma] [--out calib.json]
+
+For each producer arrangement (one DMA wave group loading A then B, and two
+loading A and B concurrently) and load path, with the calibration kernels of
+the library (``ws_gemm_create_calibration``) on the launch of an 8192 x 8192
+output (full grid, several rounds):
+
+  T_INIT      the empty kernel's time;
+  T_EPILOGUE  (epilogue-only kernel time - T_INIT) / rounds;
+  T_LOAD-A    load-only time per K-iteration of one workgroup, for two A-tile
+              sizes, from the difference of two K so that launch, fill and
+              drain cancel;
+  T_MATH      math-only time per K-iteration for the same two tiles.
+
+The two tiles of a pair run the same consumer code (128x128x64 with
+256x128x64 for one DMA group; 128x128x64 with 128x128x32 for two, whose
+largest tiles take another consumer variant).  The two-point fits of Section
+4.2 turn the pairs into throughput and startup latency.  T_LOAD-B is
+measured too and reported against the fitted line (the model assumes A and
+B loads cost the same per element).
+
+With --table, T_MATH, T_LOAD-A, T_LOAD-B and the time of loading both tiles
+(the producers' own rate, WS_CALIB_LOAD_AB) are also measured directly for
+every tile of the accuracy grid (model_eval.py), so that the event model can
+be evaluated apart from the linear cost model.  Writes one JSON document
+with every raw measurement.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import statistics
+import sys
+import time
+
+import torch
+
+from paper_2506_11209_amd import wsgemm as w
+from paper_2506_11209_amd.model import Params, params_dict, two_point_fit
+from paper_2506_11209_amd.timing import time_launches
+
+MN = 8192
+K_PAIR = (1024, 4096)
+PAIRS = {1: ((128, 128, 64), (256, 128, 64)), 2: ((128, 128, 64), (128, 128, 32))}
+TABLE_TILES = ((128, 128, 64), (256, 128, 64), (128, 256, 64), (64, 64, 64), (128, 128, 32),
+               (128, 256, 32))
+LDS_LIMIT = 163840
+
+
+def stages_for(tile):
+    tm, tn, tk = tile
+    return 3 if 256 + 3 * 2 * (tm * tk + tk * tn) <= LDS_LIMIT else 2
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_us(kind, M, N, K, tile, np_, load_path, A, B, C, steps, warmup):
+    g = w.WsGemm(M, N, K, tile, stages_for(tile), np_, 4, "bf16", load_path, calibration=kind)
+    try:
+        st = torch.cuda.current_stream().cuda_stream
+        a, b, c = A.data_ptr(), B.data_ptr(), C.data_ptr()
+        dev, _ = time_launches(lambda: g.run_ptrs(a, b, c, st), steps, warmup)
+        s = g.sync_status()
+        if s != w.WS_OK:
+            raise RuntimeError("%s: %s" % (kind, w.ws_gemm_status_str(s)))
+        return statistics.median(dev) * 1e3, g.info.rounds
+    finally:
+        g.close()
+
+
+def per_iteration_us(kind, tile, np_, load_path, bufs, steps, warmup):
+    """Time one workgroup spends per K-iteration, from two values of K."""
+    A, B, C = bufs
+    tk = tile[2]
+    t1, W = kernel_us(kind, MN, MN, K_PAIR[0], tile, np_, load_path, A, B, C, steps, warmup)
+    t2, _ = kernel_us(kind, MN, MN, K_PAIR[1], tile, np_, load_path, A, B, C, steps, warmup)
+    iters = W * (K_PAIR[1] - K_PAIR[0]) // tk
+    return (t2 - t1) / iters, {"t_k1_us": t1, "t_k2_us": t2, "rounds": W}
+
+
+def costs(tile, np_, load_path, bufs, steps, warmup):
+    """Measured per-K-iteration T_LOAD-A, T_LOAD-B and T_MATH of one tile."""
+    la, ra = per_iteration_us("load_a", tile, np_, load_path, bufs, steps, warmup)
+    lb, rb = per_iteration_us("load_b", tile, np_, load_path, bufs, steps, warmup)
+    mm, rm = per_iteration_us("math", tile, np_, load_path, bufs, steps, warmup)
+    return (la, ra), (lb, rb), (mm, rm)
+
+
+def calibrate(split, load_path, bufs, steps, warmup, table):
+    np_ = 4 * split
+    A, B, C = bufs
+    tile0 = PAIRS[split][0]
+    t_init, _ = kernel_us("empty", MN, MN, K_PAIR[0], tile0, np_, load_path, A, B, C, steps, warmup)
+    t_epi_kernel, W = kernel_us("epilogue", MN, MN, tile0[2], tile0, np_, load_path, A, B, C, steps,
+                                warmup)
+    t_epi = (t_epi_kernel - t_init) / W
+    raw = {"t_init_us": t_init, "epilogue_kernel_us": t_epi_kernel, "epilogue_rounds": W}
+    loads, loads_b, maths = [], [], []
+    for tile in PAIRS[split]:
+        tm, tn, tk = tile
+        (la, ra), (lb, rb), (mm, rm) = costs(tile, np_, load_path, bufs, steps, warmup)
+        loads.append({"tile": tile, "elements": tm * tk, "t_us": la, **ra})
+        loads_b.append({"tile": tile, "elements": tk * tn, "t_us": lb, **rb})
+        maths.append({"tile": tile, "macs": tm * tn * tk, "t_us": mm, **rm})
+        log("split %d %s tile %s: load A %.4f us, load B %.4f us, math %.4f us per K-iteration" % (
+            split, load_path, tile, la, lb, mm))
+    lt, ll = two_point_fit(loads[0]["elements"], loads[0]["t_us"], loads[1]["elements"], loads[1]["t_us"])
+    ct, cl = two_point_fit(maths[0]["macs"], maths[0]["t_us"], maths[1]["macs"], maths[1]["t_us"])
+    for rec in loads_b:
+        rec["fit_us"] = rec["elements"] / lt + ll
+    p = Params(t_init, t_epi, ct, cl, lt, ll)
+    rec = {"split": split, "load_path": load_path, "params": params_dict(p), "raw": raw,
+           "load_a": loads, "load_b": loads_b, "math": maths}
+    if table:
+        rows = []
+        for tile in TABLE_TILES:
+            (la, _), (lb, _), (mm, _) = costs(tile, np_, load_path, bufs, steps, warmup)
+            lab, _ = per_iteration_us("load_ab", tile, np_, load_path, bufs, steps, warmup)
+            rows.append({"tile": tile, "stages": stages_for(tile), "t_load_a": la, "t_load_b": lb,
+                         "t_load_ab": lab, "t_math": mm})
+            log("table split %d %s tile %s: load A %.4f  load B %.4f  load A+B %.4f  math %.4f us" % (
+                split, load_path, tile, la, lb, lab, mm))
+        rec["table"] = rows
+    return rec
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--load-paths", default="registers")
+    ap.add_argument("--splits", default="1,2")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--table", action="store_true", help="also measure every tile of the accuracy grid")
+    ap.add_argument("--out", default=None)
+    a = ap.parse_args(argv)
+    torch.manual_seed(0)
+    A = torch.randn(MN, K_PAIR[1], device="cuda").to(torch.bfloat16)
+    B = torch.randn(K_PAIR[1], MN, device="cuda").to(torch.bfloat16)
+    C = torch.empty(MN, MN, device="cuda")
+    bufs = (A, B, C)
+    # warm the clock up before the first measurement
+    g = w.WsGemm(MN, MN, K_PAIR[1], (256, 128, 64), 3, 4, 4, "bf16")
+    time_launches(lambda: g(A, B, C), 1, 50)
+    g.close()
+    out = {"device": torch.cuda.get_device_name(0), "time": time.strftime("%Y-%m-%d %H:%M:%S"),
+           "problem": {"M": MN, "N": MN, "K_pair": K_PAIR, "pairs": {str(k): v for k, v in PAIRS.items()}},
+           "calibrations": []}
+    for lp in a.load_paths.split(","):
+        for split in (int(x) for x in a.splits.split(",")):
+            rec = calibrate(split, lp, bufs, a.steps, a.warmup, a.table)
+            out["calibrations"].append(rec)
+            log("split %d %s: %s" % (split, lp, json.dumps(rec["params"])))
+    text = json.dumps(out, indent=1)
+    if a.out:
+        with open(a.out, "w") as f:
+            f.write(text + "\n")
+    print(text)
+
+
+if __name__ == "__main__":
+    main()

@@ -372,6 +372,45 @@ struct Cfg {
   static_assert(A_BYTES % 1024 == 0 && B_BYTES % 1024 == 0, "tiles must be whole KiB");
 };
 
+// What a kernel instance runs.  kModeGemm is the GEMM; the others are the
+// calibration kernels of the paper's evaluation (Section 4.2), built from the
+// same code so that they measure this kernel's own costs:
+//   kModeLoadA / kModeLoadB  the producers load only the A (B) tiles of every
+//                            K-iteration; the consumers take each slot and
+//                            release it without reading it; C is not written.
+//   kModeMath                the producers release slots without loading; the
+//                            consumers read and multiply whatever the slots
+//                            hold; C is not written.
+//   kModeEpilogue            no K loop: the consumers store one zero tile per
+//                            output tile, the producers exit.
+//   kModeLoadAB              the producers load both tiles as in the GEMM; the
+//                            consumers release every slot unread.
+enum KernelMode {
+  kModeGemm = 0, kModeLoadA = 1, kModeLoadB = 2, kModeMath = 3, kModeEpilogue = 4, kModeLoadAB = 5
+};
+
+// Epilogue: the fp32 tile of consumer wave (wm, wn) to C.  acc[mb][nb][e] is
+// row 8(e/4) + 4(lane/32) + e%4, column lane%32 of the 32x32 block.  The row
+// pitch is made opaque so that the address arithmetic stays here instead of
+// being hoisted (and spilled) out of the caller's K loop.
+template <int TM, int TN, int WM, int WN, int BM, int BN>
+__device__ __forceinline__ void store_tile(const KernelArgs& args, const f32x16_t (&acc)[BM][BN],
+                                           int ti, int tj, int wm, int wn, int lane) {
+  uint32_t ldc = (uint32_t)args.N * 4u;
+  asm volatile("" : "+s"(ldc));
+  char* cbase = (char*)args.C +
+                (((int64_t)ti * TM + wm * WM) * (int64_t)args.N + (int64_t)tj * TN + wn * WN) * 4;
+  const uint32_t lane_off = (uint32_t)(4 * (lane >> 5)) * ldc + (uint32_t)(lane & 31) * 4u;
+#pragma unroll
+  for (int mb = 0; mb < BM; ++mb)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      char* rowp = cbase + (uint32_t)(mb * 32 + 8 * (e >> 2) + (e & 3)) * ldc;
+#pragma unroll
+      for (int nb = 0; nb < BN; ++nb) *(float*)(rowp + lane_off + nb * 128) = acc[mb][nb][e];
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Per-workgroup tile sequence (identical in both roles).
 // ---------------------------------------------------------------------------
@@ -649,29 +688,53 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
   wait_vmcnt<0>();
 }
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE>
+// Producer that loads nothing: waits for each slot to be free and signals it
+// full (the calibration MATH kernel, and the idle half of a two-DMA split in
+// the load calibration kernels).
+template <int NC>
+__device__ __forceinline__ void producer_signal_only(const KernelArgs& args, WSG_LDS char* smem) {
+  WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
+  WSG_LDS uint32_t* empty = full + kMaxStages;
+  WSG_LDS uint32_t* abort_flag = full + 2 * kMaxStages;
+  const int Gd = gridDim.x;
+  const int g0 = first_slot(args);
+  const int my_tiles = g0 < args.num_tiles ? (args.num_tiles - g0 + Gd - 1) / Gd : 0;
+  const uint32_t total = (uint32_t)my_tiles * (uint32_t)args.iters;
+  const uint32_t P = (uint32_t)args.stages;
+  for (uint32_t q = 0; q < total; ++q) {
+    const uint32_t slot = q % P, use = q / P;
+    if (use > 0 && !wait_counter(&empty[slot], use * NC, abort_flag, args.spin_limit, args.err)) return;
+    lds_signal(&full[slot]);
+  }
+}
+
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B>
+__device__ __forceinline__ void producer_share(const KernelArgs& args, WSG_LDS char* smem, int a_rank,
+                                               int b_rank, int lane) {
+  if constexpr (!DO_A && !DO_B) {
+    producer_signal_only<NC>(args, smem);
+  } else if (args.load_path == 1) {  // wave-uniform: 0 = register-staged, 1 = LDS-DMA
+    producer_loop<TM, TN, TK, NC, SPLIT, BF16, TRACE, DO_A, DO_B>(args, smem, a_rank, b_rank, lane);
+  } else {
+    producer_loop_reg<TM, TN, TK, NC, SPLIT, BF16, TRACE, DO_A, DO_B>(args, smem, a_rank, b_rank, lane);
+  }
+}
+
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE>
 __device__ __forceinline__ void producer(const KernelArgs& args, WSG_LDS char* smem, int pw,
                                          int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
-  // Load path (wave-uniform): 0 = register-staged, 1 = LDS-DMA.
-  if (args.load_path == 1) {
-    if constexpr (SPLIT == 1) {
-      producer_loop<TM, TN, TK, NC, SPLIT, BF16, TRACE, true, true>(args, smem, pw, pw, lane);
-    } else {
-      if (pw < G::NP / 2)
-        producer_loop<TM, TN, TK, NC, SPLIT, BF16, TRACE, true, false>(args, smem, pw, 0, lane);
-      else
-        producer_loop<TM, TN, TK, NC, SPLIT, BF16, TRACE, false, true>(args, smem, 0, pw - G::NP / 2, lane);
-    }
+  constexpr bool LA = MODE == kModeGemm || MODE == kModeLoadA || MODE == kModeLoadAB;  // A loaded
+  constexpr bool LB = MODE == kModeGemm || MODE == kModeLoadB || MODE == kModeLoadAB;  // B loaded
+  if constexpr (MODE == kModeEpilogue) {
+    return;
+  } else if constexpr (SPLIT == 1) {
+    producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, LA, LB>(args, smem, pw, pw, lane);
   } else {
-    if constexpr (SPLIT == 1) {
-      producer_loop_reg<TM, TN, TK, NC, SPLIT, BF16, TRACE, true, true>(args, smem, pw, pw, lane);
-    } else {
-      if (pw < G::NP / 2)
-        producer_loop_reg<TM, TN, TK, NC, SPLIT, BF16, TRACE, true, false>(args, smem, pw, 0, lane);
-      else
-        producer_loop_reg<TM, TN, TK, NC, SPLIT, BF16, TRACE, false, true>(args, smem, 0, pw - G::NP / 2, lane);
-    }
+    if (pw < G::NP / 2)
+      producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, LA, false>(args, smem, pw, 0, lane);
+    else
+      producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, false, LB>(args, smem, 0, pw - G::NP / 2, lane);
   }
 }
 
@@ -708,7 +771,7 @@ struct ConsumerOps {
   }
 };
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE>
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE>
 __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* smem, int cw,
                                          int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
@@ -741,7 +804,6 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
   const uint32_t S = (uint32_t)args.iters;
   const uint32_t total = (uint32_t)my_tiles * S;
   const uint32_t P = (uint32_t)args.stages;
-  const int N = args.N;
 
   int v = g0;
   int ti, tj;
@@ -836,24 +898,10 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
     }
     ++q;
     if (++kk == S) {
-      // Epilogue: fp32 tile to C.  acc[mb][nb][e] is row 8(e/4) + 4(lane/32) + e%4,
-      // column lane%32 of the 32x32 block.  The row pitch is made opaque here
-      // so the address arithmetic stays in this block instead of being
-      // hoisted (and spilled) out of the K loop.
-      uint32_t ldc = (uint32_t)N * 4u;
-      asm volatile("" : "+s"(ldc));
-      char* cbase = (char*)args.C +
-                    (((int64_t)ti * TM + wm * G::WM) * (int64_t)N + (int64_t)tj * TN + wn * G::WN) * 4;
-      const uint32_t lane_off = (uint32_t)(4 * (lane >> 5)) * ldc + (uint32_t)(lane & 31) * 4u;
-#pragma unroll
-      for (int mb = 0; mb < G::BM; ++mb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          char* rowp = cbase + (uint32_t)(mb * 32 + 8 * (e >> 2) + (e & 3)) * ldc;
-#pragma unroll
-          for (int nb = 0; nb < G::BN; ++nb)
-            *(float*)(rowp + lane_off + nb * 128) = acc[mb][nb][e];
-        }
+      // The calibration MATH kernel keeps its products (the store below is
+      // never taken: M > 0) without writing C.
+      if (MODE != kModeMath || args.M < 0)
+        store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN>(args, acc, ti, tj, wm, wn, lane);
       if (tracing) record(q - 1, 7, cycles32());
       if (!has_next) break;
       kk = 0;
@@ -876,7 +924,7 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
 // Waits and releases are branch-free asm blocks enabled on the last k-step
 // of a K-iteration.  Same synchronisation as consumer().
 // ---------------------------------------------------------------------------
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE>
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE>
 __device__ __forceinline__ void consumer_rolling(const KernelArgs& args, WSG_LDS char* smem, int cw,
                                                  int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
@@ -903,7 +951,6 @@ __device__ __forceinline__ void consumer_rolling(const KernelArgs& args, WSG_LDS
   const uint32_t S = (uint32_t)args.iters;
   const uint32_t total = (uint32_t)my_tiles * S;
   const uint32_t P = (uint32_t)args.stages;
-  const int N = args.N;
 
   int v = g0;
   int ti, tj;
@@ -1001,20 +1048,10 @@ __device__ __forceinline__ void consumer_rolling(const KernelArgs& args, WSG_LDS
     if (nslot == 0) ntarget += (uint32_t)G::NP;
     ++q;
     if (++kk == S) {
-      uint32_t ldc = (uint32_t)N * 4u;
-      asm volatile("" : "+s"(ldc));
-      char* cbase = (char*)args.C +
-                    (((int64_t)ti * TM + wm * G::WM) * (int64_t)N + (int64_t)tj * TN + wn * G::WN) * 4;
-      const uint32_t lane_off = (uint32_t)(4 * (lane >> 5)) * ldc + (uint32_t)(lane & 31) * 4u;
-#pragma unroll
-      for (int mb = 0; mb < G::BM; ++mb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          char* rowp = cbase + (uint32_t)(mb * 32 + 8 * (e >> 2) + (e & 3)) * ldc;
-#pragma unroll
-          for (int nb = 0; nb < G::BN; ++nb)
-            *(float*)(rowp + lane_off + nb * 128) = acc[mb][nb][e];
-        }
+      // The calibration MATH kernel keeps its products (the store below is
+      // never taken: M > 0) without writing C.
+      if (MODE != kModeMath || args.M < 0)
+        store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN>(args, acc, ti, tj, wm, wn, lane);
       if (tracing) record(q - 1, 7, cycles32());
       if (!has_next) break;
       kk = 0;
@@ -1029,7 +1066,50 @@ __device__ __forceinline__ void consumer_rolling(const KernelArgs& args, WSG_LDS
   }
 }
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE>
+// Calibration consumers.  Release-only: take every slot in order and free it
+// without reading it (load calibration).  Epilogue-only: store a zero tile
+// for every output tile of the workgroup, with no K loop.
+template <int NP, int NC>
+__device__ __forceinline__ void consumer_release_only(const KernelArgs& args, WSG_LDS char* smem) {
+  WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
+  WSG_LDS uint32_t* empty = full + kMaxStages;
+  WSG_LDS uint32_t* abort_flag = full + 2 * kMaxStages;
+  const int Gd = gridDim.x;
+  const int g0 = first_slot(args);
+  const int my_tiles = g0 < args.num_tiles ? (args.num_tiles - g0 + Gd - 1) / Gd : 0;
+  const uint32_t total = (uint32_t)my_tiles * (uint32_t)args.iters;
+  const uint32_t P = (uint32_t)args.stages;
+  for (uint32_t q = 0; q < total; ++q) {
+    const uint32_t slot = q % P;
+    if (!wait_counter(&full[slot], (q / P + 1) * (uint32_t)NP, abort_flag, args.spin_limit, args.err))
+      return;
+    lds_signal(&empty[slot]);
+  }
+}
+
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16>
+__device__ __forceinline__ void consumer_epilogue_only(const KernelArgs& args, int cw, int lane) {
+  using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
+  const int wm = cw / G::WGN, wn = cw % G::WGN;
+  f32x16_t acc[G::BM][G::BN];
+#pragma unroll
+  for (int mb = 0; mb < G::BM; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < G::BN; ++nb) acc[mb][nb] = f32x16_t{};
+  for (int v = first_slot(args); v < args.num_tiles; v += (int)gridDim.x) {
+    int ti, tj;
+    tile_coords(v, args.tiles_m, args.tiles_n, args.group_m, &ti, &tj);
+    store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN>(args, acc, ti, tj, wm, wn, lane);
+  }
+}
+
+// Calibration of the launch itself (T_INIT): an empty kernel launched with
+// the GEMM's grid, block and LDS size.  A template so that every translation
+// unit including this header may instantiate it.
+template <int UNUSED = 0>
+__global__ void __launch_bounds__(1024) ws_empty_kernel(KernelArgs) {}
+
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE>
 __global__ void __launch_bounds__((NC + NC * SPLIT) * 64) ws_gemm_kernel(KernelArgs args) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
   extern __shared__ __attribute__((aligned(1024))) char smem_generic[];
@@ -1039,15 +1119,20 @@ __global__ void __launch_bounds__((NC + NC * SPLIT) * 64) ws_gemm_kernel(KernelA
   if (threadIdx.x < 2 * kMaxStages + 1) ((WSG_LDS uint32_t*)smem)[threadIdx.x] = 0u;
   __syncthreads();
   if (wave < NC) {
-    // Three waves per SIMD leave 168 VGPRs: the largest wave tiles then take
-    // the single-buffered consumer.
-    if constexpr (G::NW > 8 && G::BM * G::BN >= 8)
-      consumer_rolling<TM, TN, TK, NC, SPLIT, BF16, TRACE>(args, smem, wave, lane);
-    else
-      consumer<TM, TN, TK, NC, SPLIT, BF16, TRACE>(args, smem, wave, lane);
+    if constexpr (MODE == kModeLoadA || MODE == kModeLoadB || MODE == kModeLoadAB) {
+      consumer_release_only<G::NP, NC>(args, smem);
+    } else if constexpr (MODE == kModeEpilogue) {
+      consumer_epilogue_only<TM, TN, TK, NC, SPLIT, BF16>(args, wave, lane);
+    } else if constexpr (G::NW > 8 && G::BM * G::BN >= 8) {
+      // Three waves per SIMD leave 168 VGPRs: the largest wave tiles then
+      // take the single-buffered consumer.
+      consumer_rolling<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE>(args, smem, wave, lane);
+    } else {
+      consumer<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE>(args, smem, wave, lane);
+    }
+  } else {
+    producer<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE>(args, smem, wave - NC, lane);
   }
-  else
-    producer<TM, TN, TK, NC, SPLIT, BF16, TRACE>(args, smem, wave - NC, lane);
 }
 
 }  // namespace wsg

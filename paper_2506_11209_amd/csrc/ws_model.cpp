@@ -85,26 +85,15 @@ SimOut simulate(int64_t n, int32_t iters, int32_t stages, double t_math, double 
 
 bool positive(double x) { return x > 0.0 && isfinite(x); }
 
-}  // namespace
-
-extern "C" ws_status ws_model_predict(int64_t M, int64_t N, int64_t K, int32_t tile_m, int32_t tile_n,
-                                      int32_t tile_k, int32_t stages, int32_t slots,
-                                      const ws_model_params* p, const ws_model_options* o,
-                                      ws_model_result* out) {
-  if (!p || !out) return WS_ERR_INVALID_ARG;
-  if (M <= 0 || N <= 0 || K <= 0 || tile_m <= 0 || tile_n <= 0 || tile_k <= 0 || stages <= 0 ||
-      slots <= 0)
-    return WS_ERR_INVALID_ARG;
-  if (!positive(p->compute_throughput) || !positive(p->load_throughput)) return WS_ERR_INVALID_ARG;
+ws_status predict_core(int64_t M, int64_t N, int64_t K, int32_t tile_m, int32_t tile_n,
+                       int32_t tile_k, int32_t stages, int32_t slots, double t_math, double t_la,
+                       double t_lb, const ws_model_params* p, const ws_model_options* o,
+                       ws_model_result* out) {
   const Options opt = read_options(o);
   const int64_t tiles = ((M + tile_m - 1) / tile_m) * ((N + tile_n - 1) / tile_n);
   const int64_t W = (tiles + slots - 1) / slots;
   const int64_t S = (K + tile_k - 1) / tile_k;
   if (W > INT32_MAX || S > INT32_MAX || W * S > (int64_t)1 << 31) return WS_ERR_INVALID_ARG;
-  const double t_math =
-      (double)((int64_t)tile_m * tile_n * tile_k) / p->compute_throughput + p->compute_latency;
-  const double t_la = (double)((int64_t)tile_m * tile_k) / p->load_throughput + p->load_latency;
-  const double t_lb = (double)((int64_t)tile_k * tile_n) / p->load_throughput + p->load_latency;
   const double tail = p->t_epilogue + (opt.finish_math ? t_math : 0.0);
   ws_model_result r{};
   r.t_math = t_math;
@@ -127,6 +116,37 @@ extern "C" ws_status ws_model_predict(int64_t M, int64_t N, int64_t K, int32_t t
   }
   *out = r;
   return WS_OK;
+}
+
+bool sizes_ok(int64_t M, int64_t N, int64_t K, int32_t tile_m, int32_t tile_n, int32_t tile_k,
+              int32_t stages, int32_t slots) {
+  return M > 0 && N > 0 && K > 0 && tile_m > 0 && tile_n > 0 && tile_k > 0 && stages > 0 && slots > 0;
+}
+
+}  // namespace
+
+extern "C" ws_status ws_model_predict(int64_t M, int64_t N, int64_t K, int32_t tile_m, int32_t tile_n,
+                                      int32_t tile_k, int32_t stages, int32_t slots,
+                                      const ws_model_params* p, const ws_model_options* o,
+                                      ws_model_result* out) {
+  if (!p || !out || !sizes_ok(M, N, K, tile_m, tile_n, tile_k, stages, slots)) return WS_ERR_INVALID_ARG;
+  if (!positive(p->compute_throughput) || !positive(p->load_throughput)) return WS_ERR_INVALID_ARG;
+  const double t_math =
+      (double)((int64_t)tile_m * tile_n * tile_k) / p->compute_throughput + p->compute_latency;
+  const double t_la = (double)((int64_t)tile_m * tile_k) / p->load_throughput + p->load_latency;
+  const double t_lb = (double)((int64_t)tile_k * tile_n) / p->load_throughput + p->load_latency;
+  return predict_core(M, N, K, tile_m, tile_n, tile_k, stages, slots, t_math, t_la, t_lb, p, o, out);
+}
+
+extern "C" ws_status ws_model_predict_costs(int64_t M, int64_t N, int64_t K, int32_t tile_m,
+                                            int32_t tile_n, int32_t tile_k, int32_t stages,
+                                            int32_t slots, double t_math, double t_load_a,
+                                            double t_load_b, const ws_model_params* p,
+                                            const ws_model_options* o, ws_model_result* out) {
+  if (!p || !out || !sizes_ok(M, N, K, tile_m, tile_n, tile_k, stages, slots)) return WS_ERR_INVALID_ARG;
+  if (!isfinite(t_math) || !isfinite(t_load_a) || !isfinite(t_load_b)) return WS_ERR_INVALID_ARG;
+  return predict_core(M, N, K, tile_m, tile_n, tile_k, stages, slots, t_math, t_load_a, t_load_b, p, o,
+                      out);
 }
 
 extern "C" ws_status ws_model_events(int32_t iters, int32_t rounds, int32_t stages, double t_math,

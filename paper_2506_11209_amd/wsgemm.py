@@ -39,6 +39,13 @@ WS_ERR_HIP = 4
 WS_ERR_TIMEOUT = 5
 WS_ERR_NOT_DIVISIBLE = 6
 
+# ws_calib_kind: calibration kernels of the performance model
+WS_CALIB_NONE, WS_CALIB_EMPTY, WS_CALIB_LOAD_A, WS_CALIB_LOAD_B, WS_CALIB_MATH, WS_CALIB_EPILOGUE = \
+    -1, 0, 1, 2, 3, 4
+WS_CALIB_LOAD_AB = 5
+CALIB_KINDS = {"empty": WS_CALIB_EMPTY, "load_a": WS_CALIB_LOAD_A, "load_b": WS_CALIB_LOAD_B,
+               "math": WS_CALIB_MATH, "epilogue": WS_CALIB_EPILOGUE, "load_ab": WS_CALIB_LOAD_AB}
+
 
 class ws_gemm_config(ctypes.Structure):
     _fields_ = [("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32), ("tile_k", ctypes.c_int32),
@@ -100,6 +107,9 @@ _lib.ws_gemm_schedule.restype = _i32
 _lib.ws_gemm_create.argtypes = [_i64, _i64, _i64, ctypes.POINTER(ws_gemm_config),
                                 ctypes.POINTER(_h)]
 _lib.ws_gemm_create.restype = _i32
+_lib.ws_gemm_create_calibration.argtypes = [_i64, _i64, _i64, ctypes.POINTER(ws_gemm_config), _i32,
+                                            ctypes.POINTER(_h)]
+_lib.ws_gemm_create_calibration.restype = _i32
 _lib.ws_gemm_run.argtypes = [_h, _p, _p, _p, _p]
 _lib.ws_gemm_run.restype = _i32
 _lib.ws_gemm_sync_status.argtypes = [_h, _p]
@@ -116,6 +126,11 @@ _lib.ws_model_predict.argtypes = [_i64, _i64, _i64, _i32, _i32, _i32, _i32, _i32
                                   ctypes.POINTER(ws_model_params), ctypes.POINTER(ws_model_options),
                                   ctypes.POINTER(ws_model_result)]
 _lib.ws_model_predict.restype = _i32
+_lib.ws_model_predict_costs.argtypes = [_i64, _i64, _i64, _i32, _i32, _i32, _i32, _i32, ctypes.c_double,
+                                        ctypes.c_double, ctypes.c_double,
+                                        ctypes.POINTER(ws_model_params), ctypes.POINTER(ws_model_options),
+                                        ctypes.POINTER(ws_model_result)]
+_lib.ws_model_predict_costs.restype = _i32
 _dp = ctypes.POINTER(ctypes.c_double)
 _lib.ws_model_events.argtypes = [_i32, _i32, _i32, ctypes.c_double, ctypes.c_double, ctypes.c_double,
                                  ctypes.c_double, ctypes.POINTER(ws_model_options), _dp, _dp, _dp]
@@ -165,6 +180,12 @@ def ws_gemm_create(M, N, K, cfg: ws_gemm_config):
     return s, h
 
 
+def ws_gemm_create_calibration(M, N, K, cfg: ws_gemm_config, kind: int):
+    h = _h()
+    s = _lib.ws_gemm_create_calibration(M, N, K, ctypes.byref(cfg), kind, ctypes.byref(h))
+    return s, h
+
+
 def ws_gemm_run(h, A_ptr: int, B_ptr: int, C_ptr: int, stream_ptr: int = 0) -> int:
     return _lib.ws_gemm_run(h, _p(A_ptr), _p(B_ptr), _p(C_ptr), _p(stream_ptr))
 
@@ -204,14 +225,21 @@ class WsGemm:
     """A created plan for one (M, N, K, configuration); call it on torch tensors."""
 
     def __init__(self, M, N, K, tile=(128, 128, 32), stages=3, producer_waves=4,
-                 consumer_waves=4, dtype="bf16", load_path="registers"):
+                 consumer_waves=4, dtype="bf16", load_path="registers", calibration=None):
+        """calibration: None for the GEMM, else a key of CALIB_KINDS (the
+        calibration kernels of the performance model, same launch)."""
         self.M, self.N, self.K = M, N, K
         self.dtype = dtype
         self.cfg = config(tile, stages, producer_waves, consumer_waves, dtype, load_path)
-        s, self._h = ws_gemm_create(M, N, K, self.cfg)
+        if calibration is None:
+            s, self._h = ws_gemm_create(M, N, K, self.cfg)
+            where = "ws_gemm_create"
+        else:
+            s, self._h = ws_gemm_create_calibration(M, N, K, self.cfg, CALIB_KINDS[calibration])
+            where = "ws_gemm_create_calibration"
         if s != WS_OK:
             self._h = None
-            raise WsGemmError("ws_gemm_create", s)
+            raise WsGemmError(where, s)
         s, self.info = ws_gemm_query(self._h)
         if s != WS_OK:
             raise WsGemmError("ws_gemm_query", s)
@@ -274,6 +302,15 @@ def ws_model_predict(M, N, K, tile_m, tile_n, tile_k, stages, slots, params: ws_
     r = ws_model_result()
     s = _lib.ws_model_predict(M, N, K, tile_m, tile_n, tile_k, stages, slots, ctypes.byref(params),
                               ctypes.byref(opts) if opts is not None else None, ctypes.byref(r))
+    return s, r
+
+
+def ws_model_predict_costs(M, N, K, tile_m, tile_n, tile_k, stages, slots, t_math, t_load_a, t_load_b,
+                           params: ws_model_params, opts: ws_model_options | None = None):
+    r = ws_model_result()
+    s = _lib.ws_model_predict_costs(M, N, K, tile_m, tile_n, tile_k, stages, slots, t_math, t_load_a,
+                                    t_load_b, ctypes.byref(params),
+                                    ctypes.byref(opts) if opts is not None else None, ctypes.byref(r))
     return s, r
 
 

@@ -32,7 +32,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_text():
-    assert w.ws_gemm_abi_version() == 2
+    assert w.ws_gemm_abi_version() == 3
     for s in range(7):
         assert w.ws_gemm_status_str(s) and w.ws_gemm_status_str(s) != "unknown status"
     assert w.ws_gemm_status_str(99) == "unknown status"
@@ -171,3 +171,18 @@ def test_paper_wave_example():
         per_wg[g] = per_wg.get(g, 0) + 1
     counts = sorted(per_wg.values())
     assert counts.count(3) == vals["sms_with_3"] and counts.count(4) == vals["sms_with_4"]
+
+
+def test_calibration_kind_is_validated_before_the_device():
+    for kind in (-2, -1, 6, 99):
+        s, h = w.ws_gemm_create_calibration(256, 256, 256, cfg((64, 64, 64), 2), kind)
+        assert s == w.WS_ERR_INVALID_ARG and not h.value
+
+
+def test_calibration_needs_a_compiled_variant():
+    # calibration kernels exist for bf16 configurations with four consumer waves
+    s, h = w.ws_gemm_create_calibration(256, 256, 256, cfg((64, 64, 64), 2, dtype="f16"),
+                                        w.WS_CALIB_MATH)
+    assert s == w.WS_ERR_UNSUPPORTED and not h.value
+    s, h = w.ws_gemm_create_calibration(256, 256, 256, cfg((32, 32, 32), 2, 1, 1), w.WS_CALIB_LOAD_A)
+    assert s == w.WS_ERR_UNSUPPORTED and not h.value

@@ -296,3 +296,35 @@ def test_library_model_rejects_bad_arguments():
     assert wsgemm.ws_model_predict(64, 64, 64, 64, 64, 64, 2, 84, lib_params(1, 1, 0, 0, 1e4, 0))[0] \
         == wsgemm.WS_ERR_INVALID_ARG
     assert wsgemm.ws_model_events(0, 1, 2, 1.0, 1.0, 1.0, 0.0)[0] == wsgemm.WS_ERR_INVALID_ARG
+
+
+def test_library_predict_with_explicit_costs_matches_oracle():
+    rng = random.Random(300)
+    for two_dma in (0, 1):
+        for persistent in (0, 1):
+            opts = wsgemm.model_options(two_dma, persistent, 0)
+            for _ in range(30):
+                tm, tn, tk = 256, 128, 64
+                M, N, K = tm * rng.randint(1, 40), tn * rng.randint(1, 40), tk * rng.randint(1, 60)
+                P, slots = rng.randint(1, 6), rng.choice([84, 256])
+                t_math, t_la, t_lb = rnd_params(rng)
+                t_init, t_epi = rng.uniform(0, 10), rng.uniform(0, 5)
+                s, r = wsgemm.ws_model_predict_costs(M, N, K, tm, tn, tk, P, slots, t_math, t_la, t_lb,
+                                                     lib_params(t_init, t_epi, 1.0, 0.0, 1.0, 0.0), opts)
+                assert s == wsgemm.WS_OK
+                want = ref.overall_time(M, N, K, tm, tn, tk, P, slots, t_init, t_epi, t_math, t_la,
+                                        t_lb, two_dma=bool(two_dma),
+                                        schedule="persistent" if persistent else "per_round")
+                assert r.total_us == want
+    p = lib_params(1, 1, 1, 0, 1, 0)
+    assert wsgemm.ws_model_predict_costs(64, 64, 64, 64, 64, 64, 2, 84, float("nan"), 1.0, 1.0, p)[0] \
+        == wsgemm.WS_ERR_INVALID_ARG
+
+
+def test_package_two_point_fit_matches_oracle():
+    from paper_2506_11209_amd.model import two_point_fit
+    rng = random.Random(400)
+    for _ in range(50):
+        w1, w2 = rng.uniform(1e3, 1e6), rng.uniform(1e3, 1e6)
+        t1, t2 = rng.uniform(0.1, 10), rng.uniform(0.1, 10)
+        assert two_point_fit(w1, t1, w2, t2) == ref.two_point_fit(w1, t1, w2, t2)
