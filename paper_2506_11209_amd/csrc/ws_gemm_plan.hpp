@@ -82,10 +82,15 @@ inline int plan_launch(const PlanIn& in, PlanOut* out) {
     return kPlanInvalid;
   const int nc = in.consumer_waves, np = in.producer_waves;
   if (nc != 1 && nc != 4) return kPlanUnsupported;
-  if (np != nc && np != 2 * nc) return kPlanUnsupported;
+  // np == 0: the synchronous kernel (every wave loads and computes), ring
+  // depth 1 (no overlap) or 2 (double-buffered).
+  if (np != 0 && np != nc && np != 2 * nc) return kPlanUnsupported;
   const int wm = in.tile_m / (nc == 4 ? 2 : 1), wn = in.tile_n / (nc == 4 ? 2 : 1);
-  if (wm < 32 || wn < 32 || wm * wn > 128 * 64) return kPlanUnsupported;
-  if (in.stages < 2 || in.stages > kPlanMaxStages) return kPlanInvalid;
+  // Wave tiles hold their fp32 accumulators in registers: up to 128 x 64 when
+  // producer waves share the SIMDs, up to 128 x 128 when they do not.
+  if (wm < 32 || wn < 32 || wm * wn > (np == 0 ? 128 * 128 : 128 * 64)) return kPlanUnsupported;
+  if (np == 0 ? (in.stages < 1 || in.stages > 2) : (in.stages < 2 || in.stages > kPlanMaxStages))
+    return kPlanInvalid;
   if (in.M % in.tile_m || in.N % in.tile_n || in.K % in.tile_k) return kPlanNotDivisible;
   // element offsets inside one tile panel are 32-bit
   // byte offsets inside one tile panel (A, B and the C epilogue) are 32-bit
@@ -135,7 +140,7 @@ inline int plan_launch(const PlanIn& in, PlanOut* out) {
   out->tiles = tiles;
   out->rounds = (tiles + grid - 1) / grid;
   out->iters = (int32_t)(in.K / in.tile_k);
-  out->split = np / nc;
+  out->split = np / nc;  // 0 for the synchronous kernel
   out->group_m = best_gm;
   out->xcd_remap = xcd_remap;
   return kPlanOk;

@@ -38,6 +38,10 @@ def _sweep_8192():
         for stages in (2, 3, 4):
             for split in (1, 2):
                 pts.append(tile + (stages, 4 * split, 4))
+    # the synchronous baseline (no producer waves): ring depth 1 and 2
+    for tile in ((128, 128, 32), (128, 256, 32), (256, 128, 64), (256, 256, 64)):
+        for stages in (1, 2):
+            pts.append(tile + (stages, 0, 4))
     return tuple(pts)
 
 

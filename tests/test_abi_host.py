@@ -186,3 +186,15 @@ def test_calibration_needs_a_compiled_variant():
     assert s == w.WS_ERR_UNSUPPORTED and not h.value
     s, h = w.ws_gemm_create_calibration(256, 256, 256, cfg((32, 32, 32), 2, 1, 1), w.WS_CALIB_LOAD_A)
     assert s == w.WS_ERR_UNSUPPORTED and not h.value
+
+
+def test_plan_synchronous_kernel():
+    # producer_waves = 0: every wave loads and computes; ring depth 1 or 2
+    for P in (1, 2):
+        s, info = w.ws_gemm_plan(8192, 8192, 8192, cfg((256, 256, 64), P, 0, 4), 256, 1)
+        assert s == w.WS_OK and info.split == 0 and info.block == 256
+        assert info.lds_bytes == 256 + P * 2 * (256 * 64 + 64 * 256)
+    assert w.ws_gemm_plan(8192, 8192, 8192, cfg((256, 256, 64), 3, 0, 4), 256, 1)[0] == w.WS_ERR_INVALID_ARG
+    # 128 x 128 wave tiles only without producer waves
+    assert w.ws_gemm_plan(8192, 8192, 8192, cfg((256, 256, 32), 2, 4, 4), 256, 1)[0] == w.WS_ERR_UNSUPPORTED
+    assert w.ws_gemm_plan(1024, 1024, 1024, cfg((128, 128, 32), 1, 0, 4), 256, 1)[0] == w.WS_OK

@@ -191,7 +191,8 @@ FULL_CASES = [(name, pt, lp) for name in ("gemm_4096x4096x4096_bf16_normal",
                                           "gemm_8192x8192x8192_bf16_normal",
                                           "gemm_16384x256x8192_bf16_uniform",
                                           "gemm_2048x2048x32768_bf16_normal_k")
-              for pt in WORKLOADS[name].points for lp in ("registers", "dma")]
+              for pt in WORKLOADS[name].points for lp in ("registers", "dma")
+              if pt[4] > 0 or lp == "registers"]  # the synchronous kernel has one load path
 
 
 @pytest.mark.parametrize("name,point,load_path", FULL_CASES,
