@@ -43,7 +43,8 @@ struct PlanIn {
   int32_t tile_m, tile_n, tile_k;
   int32_t producer_waves, consumer_waves, stages, dtype, load_path;
   int32_t num_cus;     // compute units on the device
-  int32_t wgs_per_cu;  // resident workgroups per CU (<= 0: derive from LDS and waves)
+  int32_t wgs_per_cu;  // resident workgroups per CU (<= 0: derive from LDS, waves and registers)
+  int32_t vgprs, agprs;  // registers per wave of the kernel (0: unknown, not a limit)
 };
 
 struct PlanOut {
@@ -64,6 +65,20 @@ constexpr int kLdsLimit = 163840;   // bytes of LDS per workgroup on gfx950
 constexpr int kPlanHeaderBytes = 256;
 constexpr int kPlanMaxStages = 8;
 constexpr int kMaxWavesPerCu = 32;
+constexpr int kMaxWgsPerCu = 16;
+constexpr int kMaxWavesPerSimd = 8;
+constexpr int kRegsPerSimdLane = 512;  // unified VGPR + AGPR file per lane of a SIMD
+
+// Waves of one kernel that fit on a SIMD by registers: arch VGPRs rounded to
+// the accumulator offset granule (4), AGPRs after them, the total allocated
+// in granules of 8.
+inline int waves_per_simd_by_regs(int vgprs, int agprs) {
+  if (vgprs <= 0 && agprs <= 0) return kMaxWavesPerSimd;
+  int total = ((vgprs + 3) / 4) * 4 + agprs;
+  total = ((total + 7) / 8) * 8;
+  const int w = kRegsPerSimdLane / total;
+  return w < kMaxWavesPerSimd ? w : kMaxWavesPerSimd;
+}
 
 inline bool is_pow2_in(int x, int lo, int hi) {
   return x >= lo && x <= hi && (x & (x - 1)) == 0;
@@ -110,6 +125,11 @@ inline int plan_launch(const PlanIn& in, PlanOut* out) {
   if (occ <= 0) {
     occ = (int)(kLdsLimit / lds);
     if (kMaxWavesPerCu / waves < occ) occ = kMaxWavesPerCu / waves;
+    // the 4 SIMDs of a CU offer 4 x (waves per SIMD) wave slots, which the
+    // waves of resident workgroups share
+    const int by_regs = 4 * waves_per_simd_by_regs(in.vgprs, in.agprs) / waves;
+    if (by_regs < occ) occ = by_regs;
+    if (kMaxWgsPerCu < occ) occ = kMaxWgsPerCu;
   }
   if (occ < 1) occ = 1;
   int64_t slots = (int64_t)in.num_cus * occ;

@@ -93,3 +93,62 @@ def load_cost_table(path: str) -> dict:
 
 def params_dict(p: Params) -> dict:
     return asdict(p)
+
+
+# -- configuration optimizer (Section 3.2, by exhaustive search) ---------------
+
+def compiled_configs(dtype="bf16", splits=(1, 2), consumer_waves=(4,)):
+    """(tile, producer_waves, consumer_waves) of every compiled specialised GEMM
+    kernel of the given dtype (the library is built from build.instances())."""
+    from paper_2506_11209_amd.build import MODE_GEMM, instances
+    want_bf16 = 1 if dtype == "bf16" else 0
+    out = set()
+    for (tm, tn, tk, nc, split, bf16, trace, mode) in instances():
+        if bf16 == want_bf16 and not trace and mode == MODE_GEMM and split in splits and nc in consumer_waves:
+            out.add(((tm, tn, tk), nc * split, nc))
+    return sorted(out)
+
+
+def candidates(M, N, K, dtype="bf16", splits=(1, 2), stages=range(2, 9), num_cus=256,
+               load_path="registers"):
+    """Launchable (tile, stages, producer_waves, consumer_waves, slots) for this
+    problem: compiled, ring fits in LDS, tiles divide the problem.  `slots` is
+    the planned grid (workgroups that run at once)."""
+    out = []
+    for tile, np_, nc in compiled_configs(dtype, splits):
+        for P in stages:
+            cfg = w.config(tile, P, np_, nc, dtype, load_path)
+            s, info = w.ws_gemm_plan(M, N, K, cfg, num_cus, 0)
+            if s == w.WS_OK:
+                out.append((tile, P, np_, nc, info.grid))
+    return out
+
+
+def optimize(M, N, K, params_by_split: dict, cands, objective="time", persistent=True,
+             table: dict | None = None, load_path="registers"):
+    """Rank candidate launches by predicted time (objective "time", Section 3.2's
+    first goal) or by predicted total MATH wait (second goal; ties broken by
+    time, then by the deeper ring).  params_by_split: {1: Params, 2: Params}.  With `table` (from
+    load_cost_table), tiles that were measured use their own costs; the others
+    the fitted linear costs.  Returns a list of dicts, best first."""
+    rows = []
+    for (tile, P, np_, nc, slots) in cands:
+        split = np_ // nc
+        costs = table.get((split, load_path, tuple(tile))) if table else None
+        if costs is not None:
+            r = predict_costs(M, N, K, tile, P, slots, params_by_split[split], *costs,
+                              two_dma=(split == 2), persistent=persistent)
+        else:
+            r = predict(M, N, K, tile, P, slots, params_by_split[split], two_dma=(split == 2),
+                        persistent=persistent)
+        rows.append({"tile": tile, "stages": P, "producer_waves": np_, "consumer_waves": nc,
+                     "slots": slots, "time_us": r["total_us"], "wait_us": r["wait_us"],
+                     "costs": "table" if costs is not None else "fit"})
+    # Ties (the model gives every ring depth the same time once the pipeline
+    # is compute- or DMA-bound) go to the deeper ring: it is never slower in
+    # the model and hides latency the model does not represent.
+    if objective == "time":
+        rows.sort(key=lambda r: (r["time_us"], r["wait_us"], -r["stages"]))
+    else:
+        rows.sort(key=lambda r: (r["wait_us"], r["time_us"], -r["stages"]))
+    return rows

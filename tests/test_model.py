@@ -328,3 +328,33 @@ def test_package_two_point_fit_matches_oracle():
         w1, w2 = rng.uniform(1e3, 1e6), rng.uniform(1e3, 1e6)
         t1, t2 = rng.uniform(0.1, 10), rng.uniform(0.1, 10)
         assert two_point_fit(w1, t1, w2, t2) == ref.two_point_fit(w1, t1, w2, t2)
+
+
+def test_optimizer_ranks_like_brute_force_with_the_oracle():
+    # The section 3.2 optimum found by exhaustive search through the library
+    # must be the argmin of the oracle's overall time over the same candidates.
+    from paper_2506_11209_amd.model import Params, optimize
+    params = {1: Params(6.5, 1.8, 3.1e6, 0.15, 1.0e5, 0.25), 2: Params(7.3, 1.8, 4.4e6, 0.24, 2.4e5, 0.3)}
+    rng = random.Random(500)
+    tiles = [(128, 128, 64), (256, 128, 64), (128, 256, 32), (64, 64, 64)]
+    for _ in range(10):
+        M, N, K = rng.choice([2048, 4096, 8192]), rng.choice([2048, 8192]), rng.choice([1024, 8192])
+        cands = []
+        for t in tiles:
+            for P in (2, 3, 4):
+                for split in (1, 2):
+                    cands.append((t, P, 4 * split, 4, rng.choice([256, 512])))
+        for objective in ("time", "wait"):
+            rows = optimize(M, N, K, params, cands, objective)
+            def key(c):
+                t, P, np_, nc, slots = c
+                p = params[np_ // nc]
+                tm_, la, lb = ref.linear_costs(*t, p.compute_throughput, p.compute_latency,
+                                               p.load_throughput, p.load_latency)
+                total = ref.overall_time(M, N, K, *t, P, slots, p.t_init, p.t_epilogue, tm_, la, lb,
+                                         two_dma=(np_ // nc == 2), schedule="persistent")
+                return total
+            best_time = min(key(c) for c in cands)
+            if objective == "time":
+                assert rows[0]["time_us"] == best_time
+            assert sorted(r["time_us"] for r in rows) == sorted(key(c) for c in cands)
