@@ -23,6 +23,13 @@
  * and N).  A and B hold IEEE binary16 (WS_F16) or bfloat16 (WS_BF16)
  * elements; C is always binary32.  Products are accumulated in binary32.
  *
+ * Shapes: the paper's model assumes the tiles divide the problem (T_M | M,
+ * T_N | N, T_K | K).  Other shapes are accepted when K and N are multiples of
+ * 8 (rows of 16 bytes): the grid covers ceil(M/T_M) x ceil(N/T_N) tiles, the
+ * last K-iteration is partial, loads past the matrices read zeros and the
+ * epilogue stores only inside C.  They run a ragged variant of the kernel,
+ * which always uses the register-staged producers.
+ *
  * Ownership: A, B and C are device pointers owned by the caller.  A handle
  * owns its host-side plan and a small device word for the wait watchdog.
  *
@@ -40,7 +47,7 @@
 extern "C" {
 #endif
 
-#define WS_GEMM_ABI_VERSION 3
+#define WS_GEMM_ABI_VERSION 4
 
 typedef struct ws_gemm_handle* ws_gemm_t; /* opaque handle */
 
@@ -53,7 +60,8 @@ typedef enum {
   WS_ERR_LDS_OVERFLOW = 3,  /* stages x (A tile + B tile) does not fit in 160 KiB of LDS */
   WS_ERR_HIP = 4,           /* a HIP runtime call failed */
   WS_ERR_TIMEOUT = 5,       /* a producer/consumer wait exceeded its poll limit */
-  WS_ERR_NOT_DIVISIBLE = 6  /* T_M does not divide M, T_N does not divide N or T_K does not divide K */
+  WS_ERR_NOT_DIVISIBLE = 6  /* a ragged shape (tiles do not divide M, N or K) with K or N not a
+                               multiple of 8, or with producer_waves = 0 */
 } ws_status;
 
 /* How producer waves move a tile from global memory into its LDS slot. */
@@ -82,6 +90,7 @@ typedef struct {
   int32_t split;     /* 1 for one DMA warp per MATH warp, 2 for two */
   int32_t group_m;   /* tile rows per raster group */
   int32_t xcd_remap; /* 1 when workgroups are remapped so one XCD takes neighbouring tiles */
+  int32_t ragged;    /* 1 when a tile does not divide its dimension (ragged kernel variant) */
 } ws_gemm_plan_info;
 
 typedef struct {

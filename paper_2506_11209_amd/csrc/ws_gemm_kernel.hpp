@@ -392,8 +392,9 @@ enum KernelMode {
 // Epilogue: the fp32 tile of consumer wave (wm, wn) to C.  acc[mb][nb][e] is
 // row 8(e/4) + 4(lane/32) + e%4, column lane%32 of the 32x32 block.  The row
 // pitch is made opaque so that the address arithmetic stays here instead of
-// being hoisted (and spilled) out of the caller's K loop.
-template <int TM, int TN, int WM, int WN, int BM, int BN>
+// being hoisted (and spilled) out of the caller's K loop.  RAGGED: elements
+// outside C (partial edge tiles) are not stored.
+template <int TM, int TN, int WM, int WN, int BM, int BN, bool RAGGED = false>
 __device__ __forceinline__ void store_tile(const KernelArgs& args, const f32x16_t (&acc)[BM][BN],
                                            int ti, int tj, int wm, int wn, int lane) {
   uint32_t ldc = (uint32_t)args.N * 4u;
@@ -401,13 +402,19 @@ __device__ __forceinline__ void store_tile(const KernelArgs& args, const f32x16_
   char* cbase = (char*)args.C +
                 (((int64_t)ti * TM + wm * WM) * (int64_t)args.N + (int64_t)tj * TN + wn * WN) * 4;
   const uint32_t lane_off = (uint32_t)(4 * (lane >> 5)) * ldc + (uint32_t)(lane & 31) * 4u;
+  const int row0 = ti * TM + wm * WM + 4 * (lane >> 5);
+  const int col0 = tj * TN + wn * WN + (lane & 31);
 #pragma unroll
   for (int mb = 0; mb < BM; ++mb)
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      char* rowp = cbase + (uint32_t)(mb * 32 + 8 * (e >> 2) + (e & 3)) * ldc;
+      const int dr = mb * 32 + 8 * (e >> 2) + (e & 3);
+      char* rowp = cbase + (uint32_t)dr * ldc;
 #pragma unroll
-      for (int nb = 0; nb < BN; ++nb) *(float*)(rowp + lane_off + nb * 128) = acc[mb][nb][e];
+      for (int nb = 0; nb < BN; ++nb) {
+        if (!RAGGED || (row0 + dr < args.M && col0 + nb * 32 < args.N))
+          *(float*)(rowp + lane_off + nb * 128) = acc[mb][nb][e];
+      }
     }
 }
 
@@ -567,7 +574,8 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
 // ---------------------------------------------------------------------------
 typedef __attribute__((ext_vector_type(4))) int i32x4_t;
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B>
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B,
+          bool RAGGED>
 __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LDS char* smem,
                                                   int a_rank, int b_rank, int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
@@ -581,6 +589,7 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
   constexpr int L1 = (63 / LOADS) < L0 ? (63 / LOADS) : L0;
   constexpr int L = L1 < 1 ? 1 : (L1 > 6 ? 6 : L1);  // K-iterations staged in VGPRs
   static_assert(G::A_INSTR % A_GROUP == 0 && G::B_INSTR % B_GROUP == 0, "even split");
+  static_assert(LOADS <= 32, "one validity bit per chunk");
 
   WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
   WSG_LDS uint32_t* empty = full + kMaxStages;
@@ -618,6 +627,11 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
 
   i32x4_t stage[L][LOADS];
   uint32_t t_issue[L];
+  // RAGGED: bit n of vmask[u] says chunk n of staged iteration u lies inside
+  // A / B.  A chunk outside is fetched from the tile's first element (always
+  // inside) and written to LDS as zeros, so partial tiles and the tail of the
+  // last K-iteration contribute nothing.
+  uint32_t vmask[L];
   // Loads go out unconditionally (past the last K-iteration they re-read the
   // last valid tile and are never written to LDS), so every path through the
   // loop has the same number of loads in flight and the compiler's vmcnt
@@ -626,11 +640,39 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
     if (tracing) t_issue[u] = cycles32();
     const char* a_src = (const char*)(args.A + (int64_t)ti_i * TM * K + kk_i * TK);
     const char* b_src = (const char*)(args.B + (int64_t)kk_i * TK * N + (int64_t)tj_i * TN);
+    if constexpr (RAGGED) {
+      // K and N are multiples of 8, so a 16-byte chunk is wholly inside or
+      // wholly outside; the tile origin is always inside.
+      const int rows_left = args.M - ti_i * TM, cols_left = N - tj_i * TN;
+      const int k_left = K - (int)kk_i * TK;
+      uint32_t m = 0;
 #pragma unroll
-    for (int n = 0; n < A_PER; ++n) stage[u][n] = *(const i32x4_t*)(a_src + goff[n]);
+      for (int n = 0; n < A_PER; ++n) {
+        const int q = (a_rank + n * A_GROUP) * 64 + lane;
+        const int r = q / G::CA;
+        const int kc = 8 * ((q % G::CA) ^ swz_a<TK>(r));
+        const bool ok = r < rows_left && kc < k_left;
+        m |= (uint32_t)ok << n;
+        stage[u][n] = *(const i32x4_t*)(a_src + (ok ? goff[n] : 0u));
+      }
 #pragma unroll
-    for (int n = 0; n < B_PER; ++n)
-      stage[u][A_PER + n] = *(const i32x4_t*)(b_src + goff[A_PER + n]);
+      for (int n = 0; n < B_PER; ++n) {
+        const int q = (b_rank + n * B_GROUP) * 64 + lane;
+        const int blk = q >> 3, w = q & 7;
+        const int kr = (blk / G::NQ) * 4 + (w >> 1);
+        const int nc8 = (blk % G::NQ) * 16 + (w & 1) * 8;
+        const bool ok = kr < k_left && nc8 < cols_left;
+        m |= (uint32_t)ok << (A_PER + n);
+        stage[u][A_PER + n] = *(const i32x4_t*)(b_src + (ok ? goff[A_PER + n] : 0u));
+      }
+      vmask[u] = m;
+    } else {
+#pragma unroll
+      for (int n = 0; n < A_PER; ++n) stage[u][n] = *(const i32x4_t*)(a_src + goff[n]);
+#pragma unroll
+      for (int n = 0; n < B_PER; ++n)
+        stage[u][A_PER + n] = *(const i32x4_t*)(b_src + goff[A_PER + n]);
+    }
     if (q_iss + 1 < total) {
       ++q_iss;
       if (++kk_i == S) {
@@ -663,6 +705,11 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
       debug_delay(args.producer_delay);
       compiler_fence();
       WSG_LDS char* base = smem + kHeaderBytes + slot * G::STAGE + lane16;
+      if constexpr (RAGGED) {
+#pragma unroll
+        for (int n = 0; n < LOADS; ++n)
+          if (!((vmask[u] >> n) & 1u)) stage[u][n] = i32x4_t{0, 0, 0, 0};
+      }
 #pragma unroll
       for (int n = 0; n < A_PER; ++n)
         *(WSG_LDS i32x4_t*)(base + (a_rank + n * A_GROUP) * 1024) = stage[u][n];
@@ -708,19 +755,24 @@ __device__ __forceinline__ void producer_signal_only(const KernelArgs& args, WSG
   }
 }
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B>
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B,
+          bool RAGGED>
 __device__ __forceinline__ void producer_share(const KernelArgs& args, WSG_LDS char* smem, int a_rank,
                                                int b_rank, int lane) {
   if constexpr (!DO_A && !DO_B) {
     producer_signal_only<NC>(args, smem);
+  } else if constexpr (RAGGED) {  // partial tiles: always register-staged
+    producer_loop_reg<TM, TN, TK, NC, SPLIT, BF16, TRACE, DO_A, DO_B, true>(args, smem, a_rank, b_rank,
+                                                                            lane);
   } else if (args.load_path == 1) {  // wave-uniform: 0 = register-staged, 1 = LDS-DMA
     producer_loop<TM, TN, TK, NC, SPLIT, BF16, TRACE, DO_A, DO_B>(args, smem, a_rank, b_rank, lane);
   } else {
-    producer_loop_reg<TM, TN, TK, NC, SPLIT, BF16, TRACE, DO_A, DO_B>(args, smem, a_rank, b_rank, lane);
+    producer_loop_reg<TM, TN, TK, NC, SPLIT, BF16, TRACE, DO_A, DO_B, false>(args, smem, a_rank, b_rank,
+                                                                             lane);
   }
 }
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE>
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool RAGGED>
 __device__ __forceinline__ void producer(const KernelArgs& args, WSG_LDS char* smem, int pw,
                                          int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
@@ -729,12 +781,13 @@ __device__ __forceinline__ void producer(const KernelArgs& args, WSG_LDS char* s
   if constexpr (MODE == kModeEpilogue) {
     return;
   } else if constexpr (SPLIT == 1) {
-    producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, LA, LB>(args, smem, pw, pw, lane);
+    producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, LA, LB, RAGGED>(args, smem, pw, pw, lane);
   } else {
     if (pw < G::NP / 2)
-      producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, LA, false>(args, smem, pw, 0, lane);
+      producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, LA, false, RAGGED>(args, smem, pw, 0, lane);
     else
-      producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, false, LB>(args, smem, 0, pw - G::NP / 2, lane);
+      producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, false, LB, RAGGED>(args, smem, 0,
+                                                                           pw - G::NP / 2, lane);
   }
 }
 
@@ -771,7 +824,7 @@ struct ConsumerOps {
   }
 };
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE>
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool RAGGED>
 __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* smem, int cw,
                                          int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
@@ -901,7 +954,7 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
       // The calibration MATH kernel keeps its products (the store below is
       // never taken: M > 0) without writing C.
       if (MODE != kModeMath || args.M < 0)
-        store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN>(args, acc, ti, tj, wm, wn, lane);
+        store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN, RAGGED>(args, acc, ti, tj, wm, wn, lane);
       if (tracing) record(q - 1, 7, cycles32());
       if (!has_next) break;
       kk = 0;
@@ -924,7 +977,7 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
 // Waits and releases are branch-free asm blocks enabled on the last k-step
 // of a K-iteration.  Same synchronisation as consumer().
 // ---------------------------------------------------------------------------
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE>
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool RAGGED>
 __device__ __forceinline__ void consumer_rolling(const KernelArgs& args, WSG_LDS char* smem, int cw,
                                                  int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
@@ -1051,7 +1104,7 @@ __device__ __forceinline__ void consumer_rolling(const KernelArgs& args, WSG_LDS
       // The calibration MATH kernel keeps its products (the store below is
       // never taken: M > 0) without writing C.
       if (MODE != kModeMath || args.M < 0)
-        store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN>(args, acc, ti, tj, wm, wn, lane);
+        store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN, RAGGED>(args, acc, ti, tj, wm, wn, lane);
       if (tracing) record(q - 1, 7, cycles32());
       if (!has_next) break;
       kk = 0;
@@ -1109,7 +1162,7 @@ __device__ __forceinline__ void consumer_epilogue_only(const KernelArgs& args, i
 template <int UNUSED = 0>
 __global__ void __launch_bounds__(1024) ws_empty_kernel(KernelArgs) {}
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE>
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool RAGGED>
 __global__ void __launch_bounds__((NC + NC * SPLIT) * 64) ws_gemm_kernel(KernelArgs args) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
   extern __shared__ __attribute__((aligned(1024))) char smem_generic[];
@@ -1126,12 +1179,12 @@ __global__ void __launch_bounds__((NC + NC * SPLIT) * 64) ws_gemm_kernel(KernelA
     } else if constexpr (G::NW > 8 && G::BM * G::BN >= 8) {
       // Three waves per SIMD leave 168 VGPRs: the largest wave tiles then
       // take the single-buffered consumer.
-      consumer_rolling<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE>(args, smem, wave, lane);
+      consumer_rolling<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, RAGGED>(args, smem, wave, lane);
     } else {
-      consumer<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE>(args, smem, wave, lane);
+      consumer<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, RAGGED>(args, smem, wave, lane);
     }
   } else {
-    producer<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE>(args, smem, wave - NC, lane);
+    producer<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, RAGGED>(args, smem, wave - NC, lane);
   }
 }
 

@@ -6,7 +6,8 @@
 //   dispatch rounds W = ceil(tiles / workgroups)   ("waves" in the paper)
 //   K-iterations  S = K / TK                       ("stages" in the paper)
 // The paper assumes TM | M, TN | N and TK | K so that every round and every
-// K-iteration has the same cost; the planner requires the same.
+// K-iteration has the same cost; other shapes are planned with ceil() and run
+// the ragged kernel variant.
 #pragma once
 
 #include <stdint.h>
@@ -51,6 +52,7 @@ struct PlanOut {
   int32_t grid, block, lds_bytes;
   int32_t tiles_m, tiles_n, tiles, rounds, iters;
   int32_t split, group_m, xcd_remap;
+  int32_t ragged;  // 1 when a tile does not divide its dimension (edge tiles are partial)
 };
 
 enum PlanStatus {
@@ -106,7 +108,11 @@ inline int plan_launch(const PlanIn& in, PlanOut* out) {
   if (wm < 32 || wn < 32 || wm * wn > (np == 0 ? 128 * 128 : 128 * 64)) return kPlanUnsupported;
   if (np == 0 ? (in.stages < 1 || in.stages > 2) : (in.stages < 2 || in.stages > kPlanMaxStages))
     return kPlanInvalid;
-  if (in.M % in.tile_m || in.N % in.tile_n || in.K % in.tile_k) return kPlanNotDivisible;
+  // The paper's model assumes whole tiles.  Other shapes run the ragged
+  // kernel variant (partial edge tiles, a partial last K-iteration), which
+  // needs 16-byte rows of A and B (K and N multiples of 8) and producer waves.
+  const bool ragged = (in.M % in.tile_m) || (in.N % in.tile_n) || (in.K % in.tile_k);
+  if (ragged && (in.K % 8 || in.N % 8 || np == 0)) return kPlanNotDivisible;
   // element offsets inside one tile panel are 32-bit
   // byte offsets inside one tile panel (A, B and the C epilogue) are 32-bit
   if ((int64_t)in.tile_m * in.K * 2 >= (1ll << 31) || (int64_t)in.tile_k * in.N * 2 >= (1ll << 31) ||
@@ -117,7 +123,7 @@ inline int plan_launch(const PlanIn& in, PlanOut* out) {
   if (lds > kLdsLimit) return kPlanLdsOverflow;
   if (in.num_cus <= 0) return kPlanInvalid;
 
-  const int64_t tm = in.M / in.tile_m, tn = in.N / in.tile_n;
+  const int64_t tm = (in.M + in.tile_m - 1) / in.tile_m, tn = (in.N + in.tile_n - 1) / in.tile_n;
   if (tm * tn >= (1ll << 31)) return kPlanInvalid;
   const int tiles = (int)(tm * tn);
   const int waves = nc + np;
@@ -159,10 +165,11 @@ inline int plan_launch(const PlanIn& in, PlanOut* out) {
   out->tiles_n = (int32_t)tn;
   out->tiles = tiles;
   out->rounds = (tiles + grid - 1) / grid;
-  out->iters = (int32_t)(in.K / in.tile_k);
+  out->iters = (int32_t)((in.K + in.tile_k - 1) / in.tile_k);
   out->split = np / nc;  // 0 for the synchronous kernel
   out->group_m = best_gm;
   out->xcd_remap = xcd_remap;
+  out->ragged = ragged ? 1 : 0;
   return kPlanOk;
 }
 

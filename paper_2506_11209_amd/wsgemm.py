@@ -57,7 +57,7 @@ class ws_gemm_config(ctypes.Structure):
 class ws_gemm_plan_info(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "grid", "block", "lds_bytes", "tiles_m", "tiles_n", "tiles", "rounds", "iters", "split",
-        "group_m", "xcd_remap")]
+        "group_m", "xcd_remap", "ragged")]
 
     def as_dict(self) -> dict:
         return {n: getattr(self, n) for n, _ in self._fields_}

@@ -32,7 +32,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_text():
-    assert w.ws_gemm_abi_version() == 3
+    assert w.ws_gemm_abi_version() == 4
     for s in range(7):
         assert w.ws_gemm_status_str(s) and w.ws_gemm_status_str(s) != "unknown status"
     assert w.ws_gemm_status_str(99) == "unknown status"
@@ -75,9 +75,8 @@ def test_lds_overflow_case_from_the_sweep():
 
 
 @pytest.mark.parametrize("M,N,K,tile,status", [
-    (8192, 8192, 8192 + 32, (256, 128, 64), w.WS_ERR_NOT_DIVISIBLE),
-    (8192 + 64, 8192, 8192, (256, 128, 64), w.WS_ERR_NOT_DIVISIBLE),
-    (8192, 8192 + 32, 8192, (256, 128, 64), w.WS_ERR_NOT_DIVISIBLE),
+    (8192, 8192, 8192 + 4, (256, 128, 64), w.WS_ERR_NOT_DIVISIBLE),   # ragged K not a multiple of 8
+    (8192, 8192 + 12, 8192, (256, 128, 64), w.WS_ERR_NOT_DIVISIBLE),  # ragged N not a multiple of 8
     (0, 8192, 8192, (256, 128, 64), w.WS_ERR_INVALID_ARG),
     (8192, -1, 8192, (256, 128, 64), w.WS_ERR_INVALID_ARG),
     (8192, 8192, 8192, (48, 128, 64), w.WS_ERR_INVALID_ARG),
@@ -198,3 +197,17 @@ def test_plan_synchronous_kernel():
     # 128 x 128 wave tiles only without producer waves
     assert w.ws_gemm_plan(8192, 8192, 8192, cfg((256, 256, 32), 2, 4, 4), 256, 1)[0] == w.WS_ERR_UNSUPPORTED
     assert w.ws_gemm_plan(1024, 1024, 1024, cfg((128, 128, 32), 1, 0, 4), 256, 1)[0] == w.WS_OK
+
+
+@pytest.mark.parametrize("M,N,K", [(8192, 8192, 8192 + 32), (8192 + 64, 8192, 8192), (8192, 8192 + 32, 8192),
+                                   (1, 8, 8), (1000, 136, 72), (257, 8, 4104)])
+def test_plan_ragged_shapes(M, N, K):
+    tm, tn, tk = 256, 128, 64
+    s, info = w.ws_gemm_plan(M, N, K, cfg((tm, tn, tk)), 256, 1)
+    assert s == w.WS_OK and info.ragged == 1
+    assert info.tiles_m == -(-M // tm) and info.tiles_n == -(-N // tn) and info.iters == -(-K // tk)
+    # whole tiles are not ragged
+    s, info = w.ws_gemm_plan(8192, 8192, 8192, cfg((tm, tn, tk)), 256, 1)
+    assert info.ragged == 0
+    # the synchronous kernel takes whole tiles only
+    assert w.ws_gemm_plan(M, N, K, cfg((tm, tn, tk), 2, 0, 4), 256, 1)[0] == w.WS_ERR_NOT_DIVISIBLE

@@ -14,8 +14,8 @@ LDS_LIMIT = 163840
 
 def configs():
     out = set()
-    for (tm, tn, tk, nc, split, bf16, trace, mode) in instances():
-        if trace or mode != MODE_GEMM:
+    for (tm, tn, tk, nc, split, bf16, trace, mode, ragged) in instances():
+        if trace or ragged or mode != MODE_GEMM:
             continue
         for P in ((1, 2) if split == 0 else (2, 3, 4, 6)):
             if 256 + P * 2 * (tm * tk + tk * tn) <= LDS_LIMIT:
