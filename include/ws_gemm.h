@@ -21,14 +21,19 @@
  *
  * Data layout: A, B and C are dense and row-major (leading dimensions K, N
  * and N).  A and B hold IEEE binary16 (WS_F16) or bfloat16 (WS_BF16)
- * elements; C is always binary32.  Products are accumulated in binary32.
+ * elements; C is binary32 unless an epilogue says otherwise.  Products are
+ * accumulated in binary32.
+ *
+ * Epilogue: the paper's operation is C = A B.  ws_gemm_set_epilogue extends
+ * it with the BLAS form C <- alpha (A B) + beta C and a 16-bit output type;
+ * those handles run the general kernel variant (below).
  *
  * Shapes: the paper's model assumes the tiles divide the problem (T_M | M,
  * T_N | N, T_K | K).  Other shapes are accepted when K and N are multiples of
  * 8 (rows of 16 bytes): the grid covers ceil(M/T_M) x ceil(N/T_N) tiles, the
  * last K-iteration is partial, loads past the matrices read zeros and the
- * epilogue stores only inside C.  They run a ragged variant of the kernel,
- * which always uses the register-staged producers.
+ * epilogue stores only inside C.  They run the general variant of the
+ * kernel, which always uses the register-staged producers.
  *
  * Ownership: A, B and C are device pointers owned by the caller.  A handle
  * owns its host-side plan and a small device word for the wait watchdog.
@@ -47,7 +52,7 @@
 extern "C" {
 #endif
 
-#define WS_GEMM_ABI_VERSION 4
+#define WS_GEMM_ABI_VERSION 5
 
 typedef struct ws_gemm_handle* ws_gemm_t; /* opaque handle */
 
@@ -90,8 +95,23 @@ typedef struct {
   int32_t split;     /* 1 for one DMA warp per MATH warp, 2 for two */
   int32_t group_m;   /* tile rows per raster group */
   int32_t xcd_remap; /* 1 when workgroups are remapped so one XCD takes neighbouring tiles */
-  int32_t ragged;    /* 1 when a tile does not divide its dimension (ragged kernel variant) */
+  int32_t ragged;    /* 1 when a tile does not divide its dimension */
+  int32_t general;   /* 1 when the general kernel variant runs (ragged shapes, or a handle
+                        with a non-default epilogue) */
 } ws_gemm_plan_info;
+
+/* Output element type of C. */
+typedef enum { WS_OUT_F32 = 0, WS_OUT_BF16 = 1, WS_OUT_F16 = 2 } ws_out_dtype;
+
+/* Epilogue of a handle: C <- alpha (A B) + beta C, computed in binary32 as
+ * fma(beta, C, alpha * acc) and rounded once to out_dtype (round to nearest
+ * even; out of range gives infinity).  With beta == 0, C is not read (NaN in
+ * C does not propagate).  Default {1, 0, WS_OUT_F32}: the paper's C = A B. */
+typedef struct {
+  float alpha;
+  float beta;
+  int32_t out_dtype; /* ws_out_dtype; C's element type in ws_gemm_run */
+} ws_gemm_epilogue;
 
 typedef struct {
   int32_t spin_limit;     /* polls before a wait gives up (0: library default) */
@@ -129,10 +149,12 @@ ws_status ws_gemm_schedule(const ws_gemm_plan_info* info, int32_t wg, int32_t ro
 ws_status ws_gemm_create(int64_t M, int64_t N, int64_t K, const ws_gemm_config* cfg,
                          ws_gemm_t* out);
 
-/* Enqueue C = A B on `stream` (0 = the null stream).  A (M x K) and B (K x N)
- * must be 16-byte aligned device pointers, C (M x N) 4-byte aligned.  Does
- * not synchronise.  C is fully overwritten. */
-ws_status ws_gemm_run(ws_gemm_t h, const void* A, const void* B, float* C, hipStream_t stream);
+/* Enqueue C = A B (or the handle's epilogue) on `stream` (0 = the null
+ * stream).  A (M x K) and B (K x N) must be 16-byte aligned device pointers,
+ * C (M x N, element type of the epilogue's out_dtype) aligned to its element
+ * size.  Does not synchronise.  Every element of C is written; nothing
+ * outside it. */
+ws_status ws_gemm_run(ws_gemm_t h, const void* A, const void* B, void* C, hipStream_t stream);
 
 /* Synchronise `stream`, then report and clear the watchdog word:
  * WS_ERR_TIMEOUT if any wait of a previous run on this handle gave up. */
@@ -140,6 +162,15 @@ ws_status ws_gemm_sync_status(ws_gemm_t h, hipStream_t stream);
 
 /* The plan a handle launches with. */
 ws_status ws_gemm_query(ws_gemm_t h, ws_gemm_plan_info* out);
+
+/* Epilogue of later runs (NULL restores the default).  A non-default
+ * epilogue switches the handle to the general kernel variant, with its own
+ * launch (see ws_gemm_query).  WS_ERR_INVALID_ARG for a non-finite alpha or
+ * beta or an unknown out_dtype; WS_ERR_UNSUPPORTED for a non-default
+ * epilogue on a calibration handle, on a handle of the synchronous kernel
+ * (producer_waves = 0), or while tracing is on (ws_gemm_set_trace refuses a
+ * handle with a non-default epilogue likewise). */
+ws_status ws_gemm_set_epilogue(ws_gemm_t h, const ws_gemm_epilogue* epi);
 
 /* Test hooks: poll limit and injected producer/consumer delays for later
  * runs (NULL restores the defaults).  Delays force the buffer-full and

@@ -64,7 +64,7 @@ constexpr int kMaxStages = 8;
 struct KernelArgs {
   const uint16_t* A;
   const uint16_t* B;
-  float* C;
+  void* C;             // fp32, or the general variant's output type
   int32_t M, N, K;
   int32_t tiles_m, tiles_n, num_tiles;
   int32_t iters;       // S = K / TK
@@ -79,7 +79,13 @@ struct KernelArgs {
   int32_t trace_wgs;       // workgroups 0 .. trace_wgs-1 are traced
   int32_t trace_iters;     // K-iterations recorded per workgroup
   int32_t load_path;       // producer load path: 0 register-staged, 1 LDS-DMA
+  // General variant only: C <- alpha * (A B) + beta * C, C of type out_dtype.
+  float alpha, beta;
+  int32_t out_dtype;       // OutType
 };
+
+// Output element type of the general variant's epilogue.
+enum OutType { kOutF32 = 0, kOutBF16 = 1, kOutF16 = 2 };
 
 // Event trace: one record of kTraceEvents 32-bit shader-clock stamps per
 // K-iteration q of a traced workgroup (the paper's event analysis, Section
@@ -392,18 +398,30 @@ enum KernelMode {
 // Epilogue: the fp32 tile of consumer wave (wm, wn) to C.  acc[mb][nb][e] is
 // row 8(e/4) + 4(lane/32) + e%4, column lane%32 of the 32x32 block.  The row
 // pitch is made opaque so that the address arithmetic stays here instead of
-// being hoisted (and spilled) out of the caller's K loop.  RAGGED: elements
-// outside C (partial edge tiles) are not stored.
-template <int TM, int TN, int WM, int WN, int BM, int BN, bool RAGGED = false>
-__device__ __forceinline__ void store_tile(const KernelArgs& args, const f32x16_t (&acc)[BM][BN],
-                                           int ti, int tj, int wm, int wn, int lane) {
-  uint32_t ldc = (uint32_t)args.N * 4u;
+// being hoisted (and spilled) out of the caller's K loop.
+//
+// GENERAL: elements outside C (partial edge tiles) are not stored, and the
+// epilogue is the BLAS one, C <- alpha * (A B) + beta * C, rounded once to
+// the output type (round to nearest even); beta == 0 does not read C.
+template <typename T>
+__device__ __forceinline__ float load_out(const T* p) {
+  return (float)*p;
+}
+template <int TM, int TN, int WM, int WN, int BM, int BN, typename T>
+__device__ __forceinline__ void store_tile_general(const KernelArgs& args,
+                                                   const f32x16_t (&acc)[BM][BN], int ti, int tj,
+                                                   int wm, int wn, int lane) {
+  constexpr uint32_t ES = sizeof(T);
+  const float alpha = args.alpha, beta = args.beta;
+  const bool read_c = beta != 0.0f;
+  uint32_t ldc = (uint32_t)args.N * ES;
   asm volatile("" : "+s"(ldc));
-  char* cbase = (char*)args.C +
-                (((int64_t)ti * TM + wm * WM) * (int64_t)args.N + (int64_t)tj * TN + wn * WN) * 4;
-  const uint32_t lane_off = (uint32_t)(4 * (lane >> 5)) * ldc + (uint32_t)(lane & 31) * 4u;
-  const int row0 = ti * TM + wm * WM + 4 * (lane >> 5);
-  const int col0 = tj * TN + wn * WN + (lane & 31);
+  const int r0 = ti * TM + wm * WM, c0 = tj * TN + wn * WN;
+  char* cbase = (char*)args.C + ((int64_t)r0 * args.N + c0) * ES;
+  const uint32_t lane_off = (uint32_t)(4 * (lane >> 5)) * ldc + (uint32_t)(lane & 31) * ES;
+  // rows / columns of C left from this lane's first element
+  const int rows_left = args.M - r0 - 4 * (lane >> 5);
+  const int cols_left = args.N - c0 - (lane & 31);
 #pragma unroll
   for (int mb = 0; mb < BM; ++mb)
 #pragma unroll
@@ -412,10 +430,43 @@ __device__ __forceinline__ void store_tile(const KernelArgs& args, const f32x16_
       char* rowp = cbase + (uint32_t)dr * ldc;
 #pragma unroll
       for (int nb = 0; nb < BN; ++nb) {
-        if (!RAGGED || (row0 + dr < args.M && col0 + nb * 32 < args.N))
-          *(float*)(rowp + lane_off + nb * 128) = acc[mb][nb][e];
+        if (dr < rows_left && nb * 32 < cols_left) {
+          T* p = (T*)(rowp + lane_off + nb * 32 * ES);
+          float v = alpha * acc[mb][nb][e];
+          if (read_c) v = __builtin_fmaf(beta, load_out(p), v);
+          *p = (T)v;
+        }
       }
     }
+}
+
+template <int TM, int TN, int WM, int WN, int BM, int BN, bool GENERAL = false>
+__device__ __forceinline__ void store_tile(const KernelArgs& args, const f32x16_t (&acc)[BM][BN],
+                                           int ti, int tj, int wm, int wn, int lane) {
+  if constexpr (GENERAL) {
+    const int od = __builtin_amdgcn_readfirstlane(args.out_dtype);
+    if (od == kOutBF16)
+      store_tile_general<TM, TN, WM, WN, BM, BN, __bf16>(args, acc, ti, tj, wm, wn, lane);
+    else if (od == kOutF16)
+      store_tile_general<TM, TN, WM, WN, BM, BN, _Float16>(args, acc, ti, tj, wm, wn, lane);
+    else
+      store_tile_general<TM, TN, WM, WN, BM, BN, float>(args, acc, ti, tj, wm, wn, lane);
+  } else {
+    uint32_t ldc = (uint32_t)args.N * 4u;
+    asm volatile("" : "+s"(ldc));
+    char* cbase = (char*)args.C +
+                  (((int64_t)ti * TM + wm * WM) * (int64_t)args.N + (int64_t)tj * TN + wn * WN) * 4;
+    const uint32_t lane_off = (uint32_t)(4 * (lane >> 5)) * ldc + (uint32_t)(lane & 31) * 4u;
+#pragma unroll
+    for (int mb = 0; mb < BM; ++mb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int dr = mb * 32 + 8 * (e >> 2) + (e & 3);
+        char* rowp = cbase + (uint32_t)dr * ldc;
+#pragma unroll
+        for (int nb = 0; nb < BN; ++nb) *(float*)(rowp + lane_off + nb * 128) = acc[mb][nb][e];
+      }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -575,7 +626,7 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
 typedef __attribute__((ext_vector_type(4))) int i32x4_t;
 
 template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B,
-          bool RAGGED>
+          bool GENERAL>
 __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LDS char* smem,
                                                   int a_rank, int b_rank, int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
@@ -627,7 +678,7 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
 
   i32x4_t stage[L][LOADS];
   uint32_t t_issue[L];
-  // RAGGED: bit n of vmask[u] says chunk n of staged iteration u lies inside
+  // GENERAL: bit n of vmask[u] says chunk n of staged iteration u lies inside
   // A / B.  A chunk outside is fetched from the tile's first element (always
   // inside) and written to LDS as zeros, so partial tiles and the tail of the
   // last K-iteration contribute nothing.
@@ -640,7 +691,7 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
     if (tracing) t_issue[u] = cycles32();
     const char* a_src = (const char*)(args.A + (int64_t)ti_i * TM * K + kk_i * TK);
     const char* b_src = (const char*)(args.B + (int64_t)kk_i * TK * N + (int64_t)tj_i * TN);
-    if constexpr (RAGGED) {
+    if constexpr (GENERAL) {
       // K and N are multiples of 8, so a 16-byte chunk is wholly inside or
       // wholly outside; the tile origin is always inside.
       const int rows_left = args.M - ti_i * TM, cols_left = N - tj_i * TN;
@@ -705,7 +756,7 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
       debug_delay(args.producer_delay);
       compiler_fence();
       WSG_LDS char* base = smem + kHeaderBytes + slot * G::STAGE + lane16;
-      if constexpr (RAGGED) {
+      if constexpr (GENERAL) {
 #pragma unroll
         for (int n = 0; n < LOADS; ++n)
           if (!((vmask[u] >> n) & 1u)) stage[u][n] = i32x4_t{0, 0, 0, 0};
@@ -756,12 +807,12 @@ __device__ __forceinline__ void producer_signal_only(const KernelArgs& args, WSG
 }
 
 template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B,
-          bool RAGGED>
+          bool GENERAL>
 __device__ __forceinline__ void producer_share(const KernelArgs& args, WSG_LDS char* smem, int a_rank,
                                                int b_rank, int lane) {
   if constexpr (!DO_A && !DO_B) {
     producer_signal_only<NC>(args, smem);
-  } else if constexpr (RAGGED) {  // partial tiles: always register-staged
+  } else if constexpr (GENERAL) {  // partial tiles possible: always register-staged
     producer_loop_reg<TM, TN, TK, NC, SPLIT, BF16, TRACE, DO_A, DO_B, true>(args, smem, a_rank, b_rank,
                                                                             lane);
   } else if (args.load_path == 1) {  // wave-uniform: 0 = register-staged, 1 = LDS-DMA
@@ -772,7 +823,7 @@ __device__ __forceinline__ void producer_share(const KernelArgs& args, WSG_LDS c
   }
 }
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool RAGGED>
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
 __device__ __forceinline__ void producer(const KernelArgs& args, WSG_LDS char* smem, int pw,
                                          int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
@@ -781,12 +832,12 @@ __device__ __forceinline__ void producer(const KernelArgs& args, WSG_LDS char* s
   if constexpr (MODE == kModeEpilogue) {
     return;
   } else if constexpr (SPLIT == 1) {
-    producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, LA, LB, RAGGED>(args, smem, pw, pw, lane);
+    producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, LA, LB, GENERAL>(args, smem, pw, pw, lane);
   } else {
     if (pw < G::NP / 2)
-      producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, LA, false, RAGGED>(args, smem, pw, 0, lane);
+      producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, LA, false, GENERAL>(args, smem, pw, 0, lane);
     else
-      producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, false, LB, RAGGED>(args, smem, 0,
+      producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, false, LB, GENERAL>(args, smem, 0,
                                                                            pw - G::NP / 2, lane);
   }
 }
@@ -824,7 +875,7 @@ struct ConsumerOps {
   }
 };
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool RAGGED>
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
 __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* smem, int cw,
                                          int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
@@ -954,7 +1005,7 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
       // The calibration MATH kernel keeps its products (the store below is
       // never taken: M > 0) without writing C.
       if (MODE != kModeMath || args.M < 0)
-        store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN, RAGGED>(args, acc, ti, tj, wm, wn, lane);
+        store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN, GENERAL>(args, acc, ti, tj, wm, wn, lane);
       if (tracing) record(q - 1, 7, cycles32());
       if (!has_next) break;
       kk = 0;
@@ -977,7 +1028,7 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
 // Waits and releases are branch-free asm blocks enabled on the last k-step
 // of a K-iteration.  Same synchronisation as consumer().
 // ---------------------------------------------------------------------------
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool RAGGED>
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
 __device__ __forceinline__ void consumer_rolling(const KernelArgs& args, WSG_LDS char* smem, int cw,
                                                  int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
@@ -1104,7 +1155,7 @@ __device__ __forceinline__ void consumer_rolling(const KernelArgs& args, WSG_LDS
       // The calibration MATH kernel keeps its products (the store below is
       // never taken: M > 0) without writing C.
       if (MODE != kModeMath || args.M < 0)
-        store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN, RAGGED>(args, acc, ti, tj, wm, wn, lane);
+        store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN, GENERAL>(args, acc, ti, tj, wm, wn, lane);
       if (tracing) record(q - 1, 7, cycles32());
       if (!has_next) break;
       kk = 0;
@@ -1162,7 +1213,7 @@ __device__ __forceinline__ void consumer_epilogue_only(const KernelArgs& args, i
 template <int UNUSED = 0>
 __global__ void __launch_bounds__(1024) ws_empty_kernel(KernelArgs) {}
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool RAGGED>
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
 __global__ void __launch_bounds__((NC + NC * SPLIT) * 64) ws_gemm_kernel(KernelArgs args) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
   extern __shared__ __attribute__((aligned(1024))) char smem_generic[];
@@ -1179,12 +1230,12 @@ __global__ void __launch_bounds__((NC + NC * SPLIT) * 64) ws_gemm_kernel(KernelA
     } else if constexpr (G::NW > 8 && G::BM * G::BN >= 8) {
       // Three waves per SIMD leave 168 VGPRs: the largest wave tiles then
       // take the single-buffered consumer.
-      consumer_rolling<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, RAGGED>(args, smem, wave, lane);
+      consumer_rolling<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
     } else {
-      consumer<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, RAGGED>(args, smem, wave, lane);
+      consumer<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
     }
   } else {
-    producer<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, RAGGED>(args, smem, wave - NC, lane);
+    producer<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave - NC, lane);
   }
 }
 

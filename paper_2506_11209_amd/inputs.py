@@ -16,6 +16,7 @@ import numpy as np
 import torch
 
 TORCH_DTYPES = {"f16": torch.float16, "bf16": torch.bfloat16}
+OUT_DTYPES = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
 
 # value distributions
 #   int4      integers uniform on {-4, ..., 4} (inclusive)
@@ -46,6 +47,14 @@ def make_operands(M: int, N: int, K: int, dtype: str, dist: str, seed: int):
     A = _draw(M, K, dist, K, g).to(TORCH_DTYPES[dtype]).contiguous()
     B = _draw(K, N, dist, K, g).to(TORCH_DTYPES[dtype]).contiguous()
     return A, B
+
+
+def make_output(M: int, N: int, out_dtype: str, dist: str, seed: int) -> torch.Tensor:
+    """The old C read by a beta != 0 epilogue: an M x N CPU tensor of the
+    output type (f32, bf16 or f16), drawn like the operands (K = N for
+    normal_k) and rounded to nearest even."""
+    g = torch.Generator().manual_seed(seed)
+    return _draw(M, N, dist, N, g).to(OUT_DTYPES[out_dtype]).contiguous()
 
 
 def bits(t: torch.Tensor) -> np.ndarray:

@@ -57,10 +57,19 @@ class ws_gemm_config(ctypes.Structure):
 class ws_gemm_plan_info(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "grid", "block", "lds_bytes", "tiles_m", "tiles_n", "tiles", "rounds", "iters", "split",
-        "group_m", "xcd_remap", "ragged")]
+        "group_m", "xcd_remap", "ragged", "general")]
 
     def as_dict(self) -> dict:
         return {n: getattr(self, n) for n, _ in self._fields_}
+
+
+# ws_out_dtype: element type of C
+WS_OUT_F32, WS_OUT_BF16, WS_OUT_F16 = 0, 1, 2
+OUT_DTYPES = {"f32": WS_OUT_F32, "bf16": WS_OUT_BF16, "f16": WS_OUT_F16}
+
+
+class ws_gemm_epilogue(ctypes.Structure):
+    _fields_ = [("alpha", ctypes.c_float), ("beta", ctypes.c_float), ("out_dtype", ctypes.c_int32)]
 
 
 class ws_gemm_debug(ctypes.Structure):
@@ -118,6 +127,8 @@ _lib.ws_gemm_query.argtypes = [_h, ctypes.POINTER(ws_gemm_plan_info)]
 _lib.ws_gemm_query.restype = _i32
 _lib.ws_gemm_set_debug.argtypes = [_h, ctypes.POINTER(ws_gemm_debug)]
 _lib.ws_gemm_set_debug.restype = _i32
+_lib.ws_gemm_set_epilogue.argtypes = [_h, ctypes.POINTER(ws_gemm_epilogue)]
+_lib.ws_gemm_set_epilogue.restype = _i32
 _lib.ws_gemm_set_trace.argtypes = [_h, _p, _i64, _i32, _i32]
 _lib.ws_gemm_set_trace.restype = _i32
 _lib.ws_gemm_destroy.argtypes = [_h]
@@ -204,6 +215,10 @@ def ws_gemm_set_debug(h, dbg: ws_gemm_debug | None) -> int:
     return _lib.ws_gemm_set_debug(h, ctypes.byref(dbg) if dbg is not None else None)
 
 
+def ws_gemm_set_epilogue(h, epi: ws_gemm_epilogue | None) -> int:
+    return _lib.ws_gemm_set_epilogue(h, ctypes.byref(epi) if epi is not None else None)
+
+
 def ws_gemm_set_trace(h, buf_ptr: int | None, nbytes: int = 0, wgs: int = 0, iters: int = 0) -> int:
     return _lib.ws_gemm_set_trace(h, _p(buf_ptr) if buf_ptr else None, nbytes, wgs, iters)
 
@@ -230,6 +245,7 @@ class WsGemm:
         calibration kernels of the performance model, same launch)."""
         self.M, self.N, self.K = M, N, K
         self.dtype = dtype
+        self.out_dtype = "f32"
         self.cfg = config(tile, stages, producer_waves, consumer_waves, dtype, load_path)
         if calibration is None:
             s, self._h = ws_gemm_create(M, N, K, self.cfg)
@@ -256,13 +272,24 @@ class WsGemm:
         self._check(A, (self.M, self.K), self.dtype)
         self._check(B, (self.K, self.N), self.dtype)
         if C is None:
-            C = torch.empty((self.M, self.N), dtype=torch.float32, device=A.device)
-        self._check(C, (self.M, self.N), "f32")
+            want = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[self.out_dtype]
+            C = torch.empty((self.M, self.N), dtype=want, device=A.device)
+        self._check(C, (self.M, self.N), self.out_dtype)
         st = stream if stream is not None else torch.cuda.current_stream(A.device)
         s = ws_gemm_run(self._h, A.data_ptr(), B.data_ptr(), C.data_ptr(), st.cuda_stream)
         if s != WS_OK:
             raise WsGemmError("ws_gemm_run", s)
         return C
+
+    def set_epilogue(self, alpha=1.0, beta=0.0, out_dtype="f32"):
+        """C <- alpha (A B) + beta C, stored as out_dtype ("f32", "bf16", "f16")."""
+        s = ws_gemm_set_epilogue(self._h, ws_gemm_epilogue(alpha, beta, OUT_DTYPES[out_dtype]))
+        if s != WS_OK:
+            raise WsGemmError("ws_gemm_set_epilogue", s)
+        self.out_dtype = out_dtype
+        s, self.info = ws_gemm_query(self._h)
+        if s != WS_OK:
+            raise WsGemmError("ws_gemm_query", s)
 
     def run_ptrs(self, A_ptr, B_ptr, C_ptr, stream_ptr=0):
         s = ws_gemm_run(self._h, A_ptr, B_ptr, C_ptr, stream_ptr)

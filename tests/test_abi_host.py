@@ -32,7 +32,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_text():
-    assert w.ws_gemm_abi_version() == 4
+    assert w.ws_gemm_abi_version() == 5
     for s in range(7):
         assert w.ws_gemm_status_str(s) and w.ws_gemm_status_str(s) != "unknown status"
     assert w.ws_gemm_status_str(99) == "unknown status"
@@ -111,6 +111,8 @@ def test_null_handles_are_rejected():
     assert w.ws_gemm_sync_status(None, 0) == w.WS_ERR_INVALID_ARG
     assert w.ws_gemm_query(None)[0] == w.WS_ERR_INVALID_ARG
     assert w.ws_gemm_set_debug(None, None) == w.WS_ERR_INVALID_ARG
+    assert w.ws_gemm_set_epilogue(None, None) == w.WS_ERR_INVALID_ARG
+    assert w.ws_gemm_set_epilogue(None, w.ws_gemm_epilogue(2.0, 1.0, w.WS_OUT_BF16)) == w.WS_ERR_INVALID_ARG
 
 
 def _schedule(info):
@@ -204,10 +206,10 @@ def test_plan_synchronous_kernel():
 def test_plan_ragged_shapes(M, N, K):
     tm, tn, tk = 256, 128, 64
     s, info = w.ws_gemm_plan(M, N, K, cfg((tm, tn, tk)), 256, 1)
-    assert s == w.WS_OK and info.ragged == 1
+    assert s == w.WS_OK and info.ragged == 1 and info.general == 1
     assert info.tiles_m == -(-M // tm) and info.tiles_n == -(-N // tn) and info.iters == -(-K // tk)
     # whole tiles are not ragged
     s, info = w.ws_gemm_plan(8192, 8192, 8192, cfg((tm, tn, tk)), 256, 1)
-    assert info.ragged == 0
+    assert info.ragged == 0 and info.general == 0
     # the synchronous kernel takes whole tiles only
     assert w.ws_gemm_plan(M, N, K, cfg((tm, tn, tk), 2, 0, 4), 256, 1)[0] == w.WS_ERR_NOT_DIVISIBLE
