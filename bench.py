@@ -62,7 +62,7 @@ def traffic_for(point_key: str):
     return None
 
 
-def cpu_baseline(wl, target_s: float = 10.0):
+def cpu_baseline(wl, target_s: float = 15.0):
     """The oracle (fp64 triple loop, as committed) on a sample of rows of C."""
     import numpy as np
     import oracle
@@ -70,10 +70,13 @@ def cpu_baseline(wl, target_s: float = 10.0):
     A, B = inputs.make_operands(wl.M, wl.N, wl.K, wl.dtype, wl.dist, wl.seed)
     Ab, Bb = inputs.bits(A), inputs.bits(B)
     lib = oracle.load()
+    # size the sample from a probe of a few rows per thread (a probe of one
+    # row per thread is dominated by thread start-up and undersizes it)
+    cal_rows = min(wl.M, 4 * max(16, oracle.max_threads(lib)))
     t0 = time.perf_counter()
-    oracle.gemm_rows(Ab, Bb, wl.dtype, np.arange(16), lib=lib, with_abs=False)
+    oracle.gemm_rows(Ab, Bb, wl.dtype, np.arange(cal_rows), lib=lib, with_abs=False)
     t_cal = time.perf_counter() - t0
-    rows = int(max(16, min(wl.M, 16 * target_s / max(t_cal, 1e-3))))
+    rows = int(max(16, min(wl.M, cal_rows * target_s / max(t_cal, 1e-3))))
     rows -= rows % 16
     t0 = time.perf_counter()
     oracle.gemm_rows(Ab, Bb, wl.dtype, np.arange(rows), lib=lib, with_abs=False)

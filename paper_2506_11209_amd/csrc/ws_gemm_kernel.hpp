@@ -407,15 +407,21 @@ template <typename T>
 __device__ __forceinline__ float load_out(const T* p) {
   return (float)*p;
 }
-template <int TM, int TN, int WM, int WN, int BM, int BN, typename T>
+// One specialisation per output type T, READ_C (beta != 0) and MASK (the
+// wave tile crosses an edge of C).  The old C of EG consecutive k-step rows
+// is loaded before any of them is stored, so those loads overlap.
+template <int TM, int TN, int WM, int WN, int BM, int BN, int EG, typename T, bool READ_C, bool MASK>
 __device__ __forceinline__ void store_tile_general(const KernelArgs& args,
                                                    const f32x16_t (&acc)[BM][BN], int ti, int tj,
                                                    int wm, int wn, int lane) {
+  static_assert(16 % EG == 0, "row groups split the 16 accumulator rows");
   constexpr uint32_t ES = sizeof(T);
   const float alpha = args.alpha, beta = args.beta;
-  const bool read_c = beta != 0.0f;
   uint32_t ldc = (uint32_t)args.N * ES;
   asm volatile("" : "+s"(ldc));
+  // Lane-derived offsets are computed here, not hoisted into the caller's
+  // prologue and kept (or spilled) across its K loop.
+  asm volatile("" : "+v"(lane));
   const int r0 = ti * TM + wm * WM, c0 = tj * TN + wn * WN;
   char* cbase = (char*)args.C + ((int64_t)r0 * args.N + c0) * ES;
   const uint32_t lane_off = (uint32_t)(4 * (lane >> 5)) * ldc + (uint32_t)(lane & 31) * ES;
@@ -425,32 +431,67 @@ __device__ __forceinline__ void store_tile_general(const KernelArgs& args,
 #pragma unroll
   for (int mb = 0; mb < BM; ++mb)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int dr = mb * 32 + 8 * (e >> 2) + (e & 3);
-      char* rowp = cbase + (uint32_t)dr * ldc;
+    for (int e0 = 0; e0 < 16; e0 += EG) {
+      float old[EG][BN];
+      if constexpr (READ_C) {
 #pragma unroll
-      for (int nb = 0; nb < BN; ++nb) {
-        if (dr < rows_left && nb * 32 < cols_left) {
-          T* p = (T*)(rowp + lane_off + nb * 32 * ES);
-          float v = alpha * acc[mb][nb][e];
-          if (read_c) v = __builtin_fmaf(beta, load_out(p), v);
-          *p = (T)v;
+        for (int i = 0; i < EG; ++i) {
+          const int e = e0 + i, dr = mb * 32 + 8 * (e >> 2) + (e & 3);
+#pragma unroll
+          for (int nb = 0; nb < BN; ++nb) {
+            old[i][nb] = 0.0f;
+            if (!MASK || (dr < rows_left && nb * 32 < cols_left))
+              old[i][nb] = load_out((const T*)(cbase + (uint32_t)dr * ldc + lane_off + nb * 32 * ES));
+          }
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < EG; ++i) {
+        const int e = e0 + i, dr = mb * 32 + 8 * (e >> 2) + (e & 3);
+#pragma unroll
+        for (int nb = 0; nb < BN; ++nb) {
+          if (!MASK || (dr < rows_left && nb * 32 < cols_left)) {
+            float v = alpha * acc[mb][nb][e];
+            if constexpr (READ_C) v = __builtin_fmaf(beta, old[i][nb], v);
+            *(T*)(cbase + (uint32_t)dr * ldc + lane_off + nb * 32 * ES) = (T)v;
+          }
         }
       }
     }
 }
 
-template <int TM, int TN, int WM, int WN, int BM, int BN, bool GENERAL = false>
+template <int TM, int TN, int WM, int WN, int BM, int BN, int EG, typename T>
+__device__ __forceinline__ void store_tile_general_t(const KernelArgs& args,
+                                                     const f32x16_t (&acc)[BM][BN], int ti, int tj,
+                                                     int wm, int wn, int lane) {
+  const bool read_c = args.beta != 0.0f;
+  const bool mask = ti * TM + wm * WM + WM > args.M || tj * TN + wn * WN + WN > args.N;
+  if (read_c) {
+    if (mask)
+      store_tile_general<TM, TN, WM, WN, BM, BN, EG, T, true, true>(args, acc, ti, tj, wm, wn, lane);
+    else
+      store_tile_general<TM, TN, WM, WN, BM, BN, EG, T, true, false>(args, acc, ti, tj, wm, wn, lane);
+  } else {
+    if (mask)
+      store_tile_general<TM, TN, WM, WN, BM, BN, EG, T, false, true>(args, acc, ti, tj, wm, wn, lane);
+    else
+      store_tile_general<TM, TN, WM, WN, BM, BN, EG, T, false, false>(args, acc, ti, tj, wm, wn, lane);
+  }
+}
+
+// EG: k-step rows whose old C values are loaded together by the general
+// epilogue (fewer when registers are tight).
+template <int TM, int TN, int WM, int WN, int BM, int BN, bool GENERAL = false, int EG = 16>
 __device__ __forceinline__ void store_tile(const KernelArgs& args, const f32x16_t (&acc)[BM][BN],
                                            int ti, int tj, int wm, int wn, int lane) {
   if constexpr (GENERAL) {
     const int od = __builtin_amdgcn_readfirstlane(args.out_dtype);
     if (od == kOutBF16)
-      store_tile_general<TM, TN, WM, WN, BM, BN, __bf16>(args, acc, ti, tj, wm, wn, lane);
+      store_tile_general_t<TM, TN, WM, WN, BM, BN, EG, __bf16>(args, acc, ti, tj, wm, wn, lane);
     else if (od == kOutF16)
-      store_tile_general<TM, TN, WM, WN, BM, BN, _Float16>(args, acc, ti, tj, wm, wn, lane);
+      store_tile_general_t<TM, TN, WM, WN, BM, BN, EG, _Float16>(args, acc, ti, tj, wm, wn, lane);
     else
-      store_tile_general<TM, TN, WM, WN, BM, BN, float>(args, acc, ti, tj, wm, wn, lane);
+      store_tile_general_t<TM, TN, WM, WN, BM, BN, EG, float>(args, acc, ti, tj, wm, wn, lane);
   } else {
     uint32_t ldc = (uint32_t)args.N * 4u;
     asm volatile("" : "+s"(ldc));
@@ -683,6 +724,7 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
   // inside) and written to LDS as zeros, so partial tiles and the tail of the
   // last K-iteration contribute nothing.
   uint32_t vmask[L];
+  uint32_t edge = 0;  // bit u: staged iteration u touches an edge of A or B (wave-uniform)
   // Loads go out unconditionally (past the last K-iteration they re-read the
   // last valid tile and are never written to LDS), so every path through the
   // loop has the same number of loads in flight and the compiler's vmcnt
@@ -691,11 +733,21 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
     if (tracing) t_issue[u] = cycles32();
     const char* a_src = (const char*)(args.A + (int64_t)ti_i * TM * K + kk_i * TK);
     const char* b_src = (const char*)(args.B + (int64_t)kk_i * TK * N + (int64_t)tj_i * TN);
+    // GENERAL: a K-iteration whose tiles lie wholly inside A and B (the
+    // test is wave-uniform) loads as the plain kernel does; only the others
+    // mask their chunks.
+    bool interior = true;
+    int rows_left = 0, cols_left = 0, k_left = 0;
     if constexpr (GENERAL) {
+      rows_left = args.M - ti_i * TM;
+      cols_left = N - tj_i * TN;
+      k_left = K - (int)kk_i * TK;
+      interior = rows_left >= TM && cols_left >= TN && k_left >= TK;
+      edge = (edge & ~(1u << u)) | ((interior ? 0u : 1u) << u);
+    }
+    if (GENERAL && !interior) {
       // K and N are multiples of 8, so a 16-byte chunk is wholly inside or
       // wholly outside; the tile origin is always inside.
-      const int rows_left = args.M - ti_i * TM, cols_left = N - tj_i * TN;
-      const int k_left = K - (int)kk_i * TK;
       uint32_t m = 0;
 #pragma unroll
       for (int n = 0; n < A_PER; ++n) {
@@ -756,7 +808,7 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
       debug_delay(args.producer_delay);
       compiler_fence();
       WSG_LDS char* base = smem + kHeaderBytes + slot * G::STAGE + lane16;
-      if constexpr (GENERAL) {
+      if (GENERAL && ((edge >> u) & 1u)) {
 #pragma unroll
         for (int n = 0; n < LOADS; ++n)
           if (!((vmask[u] >> n) & 1u)) stage[u][n] = i32x4_t{0, 0, 0, 0};
@@ -1005,7 +1057,7 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
       // The calibration MATH kernel keeps its products (the store below is
       // never taken: M > 0) without writing C.
       if (MODE != kModeMath || args.M < 0)
-        store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN, GENERAL>(args, acc, ti, tj, wm, wn, lane);
+        store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN, GENERAL, (G::NW > 8 ? 1 : (G::BN > 2 ? 32 / G::BN : 16))>(args, acc, ti, tj, wm, wn, lane);
       if (tracing) record(q - 1, 7, cycles32());
       if (!has_next) break;
       kk = 0;
@@ -1155,7 +1207,7 @@ __device__ __forceinline__ void consumer_rolling(const KernelArgs& args, WSG_LDS
       // The calibration MATH kernel keeps its products (the store below is
       // never taken: M > 0) without writing C.
       if (MODE != kModeMath || args.M < 0)
-        store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN, GENERAL>(args, acc, ti, tj, wm, wn, lane);
+        store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN, GENERAL, 1>(args, acc, ti, tj, wm, wn, lane);
       if (tracing) record(q - 1, 7, cycles32());
       if (!has_next) break;
       kk = 0;

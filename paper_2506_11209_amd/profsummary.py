@@ -6,7 +6,9 @@
         --kernel SUBSTR --point KEY [--copy-mib 1024]
 
 `trace`: per-kernel call count, mean / median / min duration (us), from
-`rocprofv3 --kernel-trace`.  `counters`: per-kernel mean of each collected
+`rocprofv3 --kernel-trace` (with `--group G`: the matching dispatches in
+launch order cut into consecutive runs of G, one line per run, for programs
+that time one case after another).  `counters`: per-kernel mean of each collected
 counter over its dispatches (instances summed per dispatch), from
 `rocprofv3 --pmc ...`.  `traffic`: HBM bytes per launch of a kernel from
 FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by bytes-moved /
@@ -32,6 +34,16 @@ def kernel_durations(db_path: str, kernel: str | None = None, skip: int = 0):
         if kernel is None or kernel in name:
             out[name].append(dur / 1e3)  # ns -> us
     return {k: v[skip:] for k, v in out.items() if len(v) > skip}
+
+
+def dispatch_runs(db_path: str, kernel: str | None, group: int, skip: int = 0):
+    """Matching dispatches in launch order, cut into consecutive runs of
+    `group`; each run as (kernel name, durations in us after its first
+    `skip`)."""
+    db = sqlite3.connect(db_path)
+    rows = [(n, d / 1e3) for n, d in db.execute("select name, duration from kernels order by start")
+            if kernel is None or kernel in n]
+    return [(rows[i][0], [d for _, d in rows[i:i + group]][skip:]) for i in range(0, len(rows), group)]
 
 
 def counter_means(db_path: str, kernel: str | None = None):
@@ -79,13 +91,19 @@ def main(argv=None):
     ap.add_argument("--kernel", default=None)
     ap.add_argument("--point", default=None)
     ap.add_argument("--copy-mib", type=int, default=1024)
-    ap.add_argument("--skip", type=int, default=0, help="trace: leading dispatches per kernel to drop")
+    ap.add_argument("--skip", type=int, default=0, help="trace: leading dispatches per kernel (or run) to drop")
+    ap.add_argument("--group", type=int, default=0, help="trace: dispatches per consecutive run")
     a = ap.parse_args(argv)
     if a.mode == "traffic":
         traffic(*a.db[:4], a.kernel, a.point, a.copy_mib)
         return
     a.db = a.db[0]
-    if a.mode == "trace":
+    if a.mode == "trace" and a.group > 0:
+        for i, (name, d) in enumerate(dispatch_runs(a.db, a.kernel, a.group, a.skip)):
+            if d:
+                print("run %-3d %-64s n=%-4d mean_us=%.2f median_us=%.2f min_us=%.2f" % (
+                    i, name[:64], len(d), statistics.fmean(d), statistics.median(d), min(d)))
+    elif a.mode == "trace":
         for name, d in sorted(kernel_durations(a.db, a.kernel, a.skip).items(), key=lambda x: -sum(x[1])):
             print("%-72s calls=%-5d mean_us=%.2f median_us=%.2f min_us=%.2f" % (
                 name[:72], len(d), statistics.fmean(d), statistics.median(d), min(d)))
