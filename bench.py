@@ -30,27 +30,20 @@ PEAK_TFLOPS = 2500.0                      # MI355X dense bf16 MFMA
 PROFILES = os.path.join(ROOT, "profiles")
 
 
-# Sources the GEMM kernel and its launch are built from (host-only model code
-# and the like do not change the kernel's memory traffic).
-KERNEL_SOURCES = ("ws_gemm_api.cpp", "ws_gemm_kernel.hpp", "ws_gemm_plan.hpp", "ws_gemm_registry.hpp")
+def kernel_fingerprint(point=DEFAULT_POINT, dtype="bf16") -> str:
+    """Hash of the machine code of the GEMM kernel that `point` launches, read
+    from the built library (the counter records are tied to that code)."""
+    from paper_2506_11209_amd.kernel_code import gemm_symbol, kernel_fingerprint as code_fingerprint
+    tm, tn, tk, _stages, np_, nc = point
+    return code_fingerprint(gemm_symbol(tm, tn, tk, nc, np_ // nc, bf16=(dtype == "bf16")))
 
 
-def kernel_fingerprint() -> str:
-    import hashlib
-    h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2506_11209_amd", "csrc")
-    for name in KERNEL_SOURCES:
-        with open(os.path.join(csrc, name), "rb") as f:
-            h.update(name.encode() + f.read())
-    return h.hexdigest()[:16]
-
-
-def traffic_for(point_key: str):
+def traffic_for(point_key: str, point=DEFAULT_POINT):
     """HBM bytes per launch from the committed counter runs (profiles/
-    *hbm_traffic*.json), if they were taken on the current kernel sources
-    and this launch point; else None."""
+    *hbm_traffic*.json), if they were taken on this launch point and on the
+    machine code the library now holds for it; else None."""
     import glob
-    fp = kernel_fingerprint()
+    fp = kernel_fingerprint(point)
     for path in sorted(glob.glob(os.path.join(PROFILES, "*hbm_traffic*.json"))):
         try:
             with open(path) as f:
@@ -155,7 +148,7 @@ def main():
                    "load_path": a.load_path, "grid": g.info.grid, "rounds": g.info.rounds},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS, 4),
-                     "traffic": traffic_for(pkey),
+                     "traffic": traffic_for(pkey, point),
                      "kernel": "ws_gemm_kernel<%d,%d,%d,%d,%d,bf16>" % (tm, tn, tk, nc, np_ // nc),
                      "launch_ms": {k: round(v, 5) if isinstance(v, float) else v for k, v in sm.items()}},
     }

@@ -46,6 +46,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "ws_ring.hpp"
+
 #include "ws_gemm_plan.hpp"
 
 namespace wsg {
@@ -601,15 +603,14 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
     const uint16_t* a_tile = args.A + (int64_t)ti * TM * K;
     const uint16_t* b_tile = args.B + (int64_t)tj * TN;
     for (int kk = 0; kk < args.iters; ++kk, ++q) {
-      const uint32_t slot = q % P;
-      const uint32_t use = q / P;
-      if (use > 0) {
-        // wait(): the slot is free once every consumer wave released use - 1.
-        const uint32_t need = use * NC;
+      const uint32_t slot = ring_slot(q, P);
+      if (ring_use(q, P) > 0) {
+        // wait(): the slot is free once every consumer wave released its previous use.
+        const uint32_t need = ring_empty_target(q, P, NC);
         if ((int32_t)(lds_read_now(&empty[slot]) - need) < 0) {
           while (q_sig < q) {  // publish pending iterations first, oldest first
             wait_landed<LOADS>(q - q_sig - 1);
-            publish(q_sig % P);
+            publish(ring_slot(q_sig, P));
             ++q_sig;
           }
           if (!wait_counter(&empty[slot], need, abort_flag, args.spin_limit, args.err)) {
@@ -643,14 +644,14 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
       // signal(): iteration q - lag has landed once at most `lag` newer ones are in flight.
       if (q + 1 - q_sig > lag) {
         wait_landed<LOADS>(lag);
-        publish(q_sig % P);
+        publish(ring_slot(q_sig, P));
         ++q_sig;
       }
     }
   }
   while (q_sig < q) {
     wait_landed<LOADS>(q - q_sig - 1);
-    publish(q_sig % P);
+    publish(ring_slot(q_sig, P));
     ++q_sig;
   }
 }
@@ -794,10 +795,9 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
     for (int u = 0; u < L; ++u) {
       const uint32_t q = q0 + u;
       if (q < total) {
-      const uint32_t slot = q % P;
-      const uint32_t use = q / P;
-      if (use > 0) {
-        const uint32_t need = use * NC;
+      const uint32_t slot = ring_slot(q, P);
+      if (ring_use(q, P) > 0) {
+        const uint32_t need = ring_empty_target(q, P, NC);
         if ((int32_t)(lds_read_now(&empty[slot]) - need) < 0) {
           if (!wait_counter(&empty[slot], need, abort_flag, args.spin_limit, args.err)) {
             wait_vmcnt<0>();
@@ -852,8 +852,10 @@ __device__ __forceinline__ void producer_signal_only(const KernelArgs& args, WSG
   const uint32_t total = (uint32_t)my_tiles * (uint32_t)args.iters;
   const uint32_t P = (uint32_t)args.stages;
   for (uint32_t q = 0; q < total; ++q) {
-    const uint32_t slot = q % P, use = q / P;
-    if (use > 0 && !wait_counter(&empty[slot], use * NC, abort_flag, args.spin_limit, args.err)) return;
+    const uint32_t slot = ring_slot(q, P);
+    if (ring_use(q, P) > 0 &&
+        !wait_counter(&empty[slot], ring_empty_target(q, P, NC), abort_flag, args.spin_limit, args.err))
+      return;
     lds_signal(&full[slot]);
   }
 }
@@ -992,7 +994,9 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
   };
 
   // Prologue: wait for K-iteration 0 and read k-step 0.
-  if (!wait_counter(&full[0], (uint32_t)G::NP, abort_flag, args.spin_limit, args.err)) return;
+  if (!wait_counter(&full[ring_slot(0, P)], ring_full_target(0, P, G::NP), abort_flag,
+                    args.spin_limit, args.err))
+    return;
   record_ready(0, 0);
 #pragma unroll
   for (int mb = 0; mb < G::BM; ++mb) Ops::load_a(fa[mb], smem + kHeaderBytes, a_off[0], mb);
@@ -1002,14 +1006,14 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
 
   uint32_t q = 0, kk = 0;
   while (true) {
-    const uint32_t slot = q % P;
+    const uint32_t slot = ring_slot(q, P);
     WSG_LDS char* a_src = smem + kHeaderBytes + slot * G::STAGE;
     WSG_LDS char* b_src = a_src + G::A_BYTES;
     const bool has_next = (q + 1) < total;
     // After the last K-iteration the next-slot reads re-read this slot (and
     // are never used), so every path issues the same LDS operations.
-    const uint32_t nslot = has_next ? (q + 1) % P : slot;
-    const uint32_t ntarget = has_next ? ((q + 1) / P + 1) * (uint32_t)G::NP : 0u;
+    const uint32_t nslot = has_next ? ring_slot(q + 1, P) : slot;
+    const uint32_t ntarget = has_next ? ring_full_target(q + 1, P, G::NP) : 0u;
     WSG_LDS char* na_src = smem + kHeaderBytes + nslot * G::STAGE;
     WSG_LDS char* nb_src = na_src + G::A_BYTES;
     uint32_t peek = 0;
@@ -1136,13 +1140,15 @@ __device__ __forceinline__ void consumer_rolling(const KernelArgs& args, WSG_LDS
     }
   };
 
-  if (!wait_counter(&full[0], (uint32_t)G::NP, abort_flag, args.spin_limit, args.err)) return;
+  if (!wait_counter(&full[ring_slot(0, P)], ring_full_target(0, P, G::NP), abort_flag,
+                    args.spin_limit, args.err))
+    return;
   record_ready(0, 0);
   // full[] of the slot the next wait is for, read one k-step before that
   // wait.  Read here before the first operand loads, so that on every path
   // into the loop a whole k-step of loads is younger than it and the wait
   // for it does not drain them.
-  uint32_t peek = lds_peek(&full[1 % P]);
+  uint32_t peek = lds_peek(&full[ring_slot(1, P)]);
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int mb = 0; mb < G::BM; ++mb) Ops::load_a(fa[mb], smem + kHeaderBytes, a_off0, mb);
@@ -1151,10 +1157,9 @@ __device__ __forceinline__ void consumer_rolling(const KernelArgs& args, WSG_LDS
     Ops::load_b(fb[nb], smem + kHeaderBytes + G::A_BYTES, b_off, 0, nb);
 
   uint32_t q = 0, kk = 0, s = 0;
-  uint32_t slot = 0, nslot = 1 % P;
-  // full[nslot] reaches ntarget once K-iteration q + 1 has landed: that is
-  // slot use (q + 1) / P, and every producer signals once per use.
-  uint32_t ntarget = (1u / P + 1u) * (uint32_t)G::NP;
+  // (nslot, ntarget): slot and full[] target of K-iteration q + 1.
+  uint32_t slot = 0, nslot = ring_slot(1, P);
+  uint32_t ntarget = ring_full_target(1, P, G::NP);
   while (true) {
     const uint32_t last = (s == (uint32_t)G::KS - 1) ? 1u : 0u;
     const bool has_next = (q + 1) < total;
@@ -1200,8 +1205,7 @@ __device__ __forceinline__ void consumer_rolling(const KernelArgs& args, WSG_LDS
     if (tracing) record(q, 6, cycles32());
     s = 0;
     slot = nslot;
-    nslot = (nslot + 1 == P) ? 0u : nslot + 1;
-    if (nslot == 0) ntarget += (uint32_t)G::NP;
+    ring_advance(nslot, ntarget, P, G::NP);
     ++q;
     if (++kk == S) {
       // The calibration MATH kernel keeps its products (the store below is
@@ -1236,8 +1240,8 @@ __device__ __forceinline__ void consumer_release_only(const KernelArgs& args, WS
   const uint32_t total = (uint32_t)my_tiles * (uint32_t)args.iters;
   const uint32_t P = (uint32_t)args.stages;
   for (uint32_t q = 0; q < total; ++q) {
-    const uint32_t slot = q % P;
-    if (!wait_counter(&full[slot], (q / P + 1) * (uint32_t)NP, abort_flag, args.spin_limit, args.err))
+    const uint32_t slot = ring_slot(q, P);
+    if (!wait_counter(&full[slot], ring_full_target(q, P, NP), abort_flag, args.spin_limit, args.err))
       return;
     lds_signal(&empty[slot]);
   }

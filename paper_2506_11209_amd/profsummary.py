@@ -14,7 +14,7 @@ counter over its dispatches (instances summed per dispatch), from
 FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by bytes-moved /
 counter-reading of the known-size copy run by
 `python -m paper_2506_11209_amd.hbm_calibrate`; printed as the JSON record
-bench.py reads (tagged with the kernel-source fingerprint).
+bench.py reads (tagged with the fingerprint of the kernel's machine code).
 """
 from __future__ import annotations
 
@@ -72,12 +72,13 @@ def traffic(fetch_db, write_db, cal_fetch_db, cal_write_db, kernel, point, copy_
     import sys
     sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
     from bench import kernel_fingerprint
+    point_t = tuple(int(x) for x in point.split("/")[0].split("x"))
     copy_bytes = copy_mib * (1 << 20)
     f_scale = copy_bytes / (_mean_counter(cal_fetch_db, "copyBuffer", "FETCH_SIZE") * 1024)
     w_scale = copy_bytes / (_mean_counter(cal_write_db, "copyBuffer", "WRITE_SIZE") * 1024)
     fetch = _mean_counter(fetch_db, kernel, "FETCH_SIZE")
     write = _mean_counter(write_db, kernel, "WRITE_SIZE")
-    rec = {"kernel": kernel, "point": point, "kernel_fingerprint": kernel_fingerprint(),
+    rec = {"kernel": kernel, "point": point, "kernel_fingerprint": kernel_fingerprint(point_t),
            "fetch_size_kib": fetch, "write_size_kib": write,
            "fetch_scale_bytes_per_kib": f_scale * 1024, "write_scale_bytes_per_kib": w_scale * 1024,
            "traffic_bytes_per_launch": fetch * 1024 * f_scale + write * 1024 * w_scale}

@@ -1,0 +1,155 @@
+// Host model of the warp-specialised kernel's circular-buffer protocol (test
+// infrastructure; built with g++ and run under ThreadSanitizer by
+// tests/test_ring_protocol.py).
+//
+// NP producer threads and NC consumer threads stand for the producer and
+// consumer waves of one workgroup.  They walk T K-iterations through a ring
+// of P slots with the slot / counter arithmetic the kernels use
+// (paper_2506_11209_amd/csrc/ws_ring.hpp): a producer of K-iteration q waits
+// until empty[slot] reaches ring_empty_target, writes its share of the slot
+// (plain, non-atomic stores), then signals full[slot] with a release add; a
+// consumer waits until full[slot] reaches ring_full_target (acquire), reads
+// every share and checks its tags, then releases with an add on empty[slot].
+// Half of the consumers walk the ring with the closed forms, half with
+// ring_advance, as the two consumer variants of the kernel do.
+//
+// Waits are bounded (a watchdog like the kernel's, here in milliseconds of
+// waiting): on timeout the thread raises an abort flag and every thread
+// leaves at its next poll.
+//
+// Exit status: 0 all tags read as written; 1 a tag mismatch; 2 a wait timed
+// out; 3 bad arguments.  ThreadSanitizer reports races on the slot data
+// (and exits with its own status) when the ordering is wrong.
+//
+// Planted mistakes, selected with -D for the tests that must catch them:
+//   PLANT_EARLY_RELEASE  consumers release the slot before reading it
+//   PLANT_EARLY_READ     consumers wait for one producer signal too few
+//   PLANT_DROP_SIGNAL    producer 0 skips its signal of K-iteration T/2
+#include <atomic>
+#include <chrono>
+#include <cstdint>
+#include <cstdio>
+#include <cstdlib>
+#include <thread>
+#include <vector>
+
+#include "ws_ring.hpp"
+
+namespace {
+
+constexpr int kChunks = 8;  // words each producer writes per slot use
+
+struct Ring {
+  uint32_t P, NP, NC, T;
+  long long limit_ms;
+  std::vector<std::atomic<uint32_t>> full, empty;
+  std::vector<uint64_t> data;  // [P][NP][kChunks], plain memory
+  std::atomic<int> abort{0};
+  std::atomic<int> timeouts{0}, mismatches{0};
+  Ring(uint32_t p, uint32_t np, uint32_t nc, uint32_t t, long long limit)
+      : P(p), NP(np), NC(nc), T(t), limit_ms(limit), full(p), empty(p),
+        data((size_t)p * np * kChunks, 0) {
+    for (auto& c : full) c.store(0);
+    for (auto& c : empty) c.store(0);
+  }
+  uint64_t* share(uint32_t slot, uint32_t producer) {
+    return &data[((size_t)slot * NP + producer) * kChunks];
+  }
+};
+
+uint64_t tag(uint32_t q, uint32_t producer, int chunk) {
+  return ((uint64_t)q << 20) ^ ((uint64_t)producer << 8) ^ (uint64_t)chunk ^ 0x5a5a000000000000ull;
+}
+
+// true when ctr reached target; false after the watchdog (or another
+// thread's) abort.
+bool wait_for(Ring& r, std::atomic<uint32_t>& ctr, uint32_t target) {
+  const auto start = std::chrono::steady_clock::now();
+  long long spins = 0;
+  while ((int32_t)(ctr.load(std::memory_order_acquire) - target) < 0) {
+    if (r.abort.load(std::memory_order_relaxed)) return false;
+    if ((++spins & 255) == 0) {
+      const auto waited = std::chrono::steady_clock::now() - start;
+      if (std::chrono::duration_cast<std::chrono::milliseconds>(waited).count() > r.limit_ms) {
+        r.timeouts.fetch_add(1);
+        r.abort.store(1);
+        return false;
+      }
+      std::this_thread::yield();
+    }
+  }
+  return true;
+}
+
+void producer(Ring& r, uint32_t p) {
+  for (uint32_t q = 0; q < r.T; ++q) {
+    const uint32_t slot = wsg::ring_slot(q, r.P);
+    if (wsg::ring_use(q, r.P) > 0 && !wait_for(r, r.empty[slot], wsg::ring_empty_target(q, r.P, r.NC)))
+      return;
+    uint64_t* d = r.share(slot, p);
+    for (int c = 0; c < kChunks; ++c) d[c] = tag(q, p, c);
+#ifdef PLANT_DROP_SIGNAL
+    if (p == 0 && q == r.T / 2) continue;
+#endif
+    r.full[slot].fetch_add(1, std::memory_order_release);
+  }
+}
+
+void consume(Ring& r, uint32_t q, uint32_t slot, uint32_t target) {
+#ifdef PLANT_EARLY_READ
+  target -= 1;
+#endif
+  if (!wait_for(r, r.full[slot], target)) return;
+#ifdef PLANT_EARLY_RELEASE
+  r.empty[slot].fetch_add(1, std::memory_order_release);
+#endif
+  for (uint32_t p = 0; p < r.NP; ++p) {
+    const uint64_t* d = r.share(slot, p);
+    for (int c = 0; c < kChunks; ++c)
+      if (d[c] != tag(q, p, c)) r.mismatches.fetch_add(1);
+  }
+#ifndef PLANT_EARLY_RELEASE
+  r.empty[slot].fetch_add(1, std::memory_order_release);
+#endif
+}
+
+void consumer_closed_form(Ring& r) {
+  for (uint32_t q = 0; q < r.T && !r.abort.load(std::memory_order_relaxed); ++q)
+    consume(r, q, wsg::ring_slot(q, r.P), wsg::ring_full_target(q, r.P, r.NP));
+}
+
+void consumer_incremental(Ring& r) {
+  uint32_t slot = wsg::ring_slot(0, r.P), target = wsg::ring_full_target(0, r.P, r.NP);
+  for (uint32_t q = 0; q < r.T && !r.abort.load(std::memory_order_relaxed); ++q) {
+    if (slot != wsg::ring_slot(q, r.P) || target != wsg::ring_full_target(q, r.P, r.NP)) {
+      r.mismatches.fetch_add(1);  // the two walks disagree
+      return;
+    }
+    consume(r, q, slot, target);
+    wsg::ring_advance(slot, target, r.P, r.NP);
+  }
+}
+
+}  // namespace
+
+int main(int argc, char** argv) {
+  if (argc != 6) {
+    std::fprintf(stderr, "usage: %s P NP NC T WAIT_LIMIT_MS\n", argv[0]);
+    return 3;
+  }
+  const long P = std::atol(argv[1]), NP = std::atol(argv[2]), NC = std::atol(argv[3]);
+  const long T = std::atol(argv[4]);
+  const long long limit = std::atoll(argv[5]);
+  if (P < 1 || P > 64 || NP < 1 || NP > 64 || NC < 1 || NC > 64 || T < 1 || limit < 1) return 3;
+  Ring r((uint32_t)P, (uint32_t)NP, (uint32_t)NC, (uint32_t)T, limit);
+  std::vector<std::thread> th;
+  for (uint32_t p = 0; p < r.NP; ++p) th.emplace_back(producer, std::ref(r), p);
+  for (uint32_t c = 0; c < r.NC; ++c)
+    th.emplace_back((c % 2) ? consumer_incremental : consumer_closed_form, std::ref(r));
+  for (auto& t : th) t.join();
+  std::printf("P=%ld NP=%ld NC=%ld T=%ld timeouts=%d mismatches=%d\n", P, NP, NC, T, r.timeouts.load(),
+              r.mismatches.load());
+  if (r.timeouts.load()) return 2;
+  if (r.mismatches.load()) return 1;
+  return 0;
+}

@@ -1,0 +1,77 @@
+"""Host model of the circular-buffer protocol (tests/ring_protocol_model.cpp),
+built with g++ and ThreadSanitizer, over the ring arithmetic the kernels use
+(paper_2506_11209_amd/csrc/ws_ring.hpp).
+
+The correct protocol must run every configuration without a data race, a
+wrong tag or a timeout; each planted mistake must be caught: a slot released
+before it is read or read one signal early races (ThreadSanitizer) and
+returns wrong tags, and a dropped signal ends in the watchdog's timeout
+instead of a hang."""
+import os
+import shutil
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SOURCE = os.path.join(ROOT, "tests", "ring_protocol_model.cpp")
+INCLUDE = os.path.join(ROOT, "paper_2506_11209_amd", "csrc")
+
+pytestmark = pytest.mark.skipif(shutil.which("g++") is None, reason="g++ not available")
+
+TSAN_RACE_STATUS = 66  # ThreadSanitizer's exit status when it reported a race
+
+
+@pytest.fixture(scope="module")
+def models(tmp_path_factory):
+    out = tmp_path_factory.mktemp("ring_model")
+    built = {}
+    for plant in ("", "PLANT_EARLY_RELEASE", "PLANT_EARLY_READ", "PLANT_DROP_SIGNAL"):
+        exe = str(out / ("model_" + (plant or "ok")))
+        cmd = ["g++", "-std=c++17", "-O1", "-g", "-pthread", "-fsanitize=thread", "-I" + INCLUDE, SOURCE,
+               "-o", exe]
+        if plant:
+            cmd.insert(1, "-D" + plant)
+        subprocess.run(cmd, check=True)
+        built[plant] = exe
+    return built
+
+
+def run(exe, P, NP, NC, T, limit_ms=5000):
+    env = dict(os.environ, TSAN_OPTIONS="halt_on_error=0")
+    r = subprocess.run([exe, str(P), str(NP), str(NC), str(T), str(limit_ms)], capture_output=True, text=True,
+                       timeout=120, env=env)
+    return r.returncode, r.stdout + r.stderr
+
+
+# ring depths, producer / consumer wave counts of the kernel's arrangements
+# (1:1 and 2:1 with one or four consumer waves), and K-iteration counts well
+# beyond the ring depth
+CONFIGS = [(P, NP, NC, T) for (NP, NC) in ((1, 1), (2, 1), (4, 4), (8, 4)) for P in (1, 2, 3, 8)
+           for T in (1, 7, 1500)]
+
+
+@pytest.mark.parametrize("P,NP,NC,T", CONFIGS)
+def test_protocol_is_race_free_and_delivers_every_tile(models, P, NP, NC, T):
+    rc, out = run(models[""], P, NP, NC, T)
+    assert rc == 0, out
+    assert "ThreadSanitizer" not in out, out
+
+
+@pytest.mark.parametrize("P,NP,NC", [(2, 4, 4), (3, 8, 4), (1, 1, 1)])
+def test_early_release_is_caught(models, P, NP, NC):
+    rc, out = run(models["PLANT_EARLY_RELEASE"], P, NP, NC, 2000)
+    assert rc == TSAN_RACE_STATUS and "data race" in out, out
+
+
+@pytest.mark.parametrize("P,NP,NC", [(2, 4, 4), (3, 8, 4), (1, 1, 1)])
+def test_early_read_is_caught(models, P, NP, NC):
+    rc, out = run(models["PLANT_EARLY_READ"], P, NP, NC, 2000)
+    assert rc == TSAN_RACE_STATUS and "data race" in out, out
+
+
+@pytest.mark.parametrize("P,NP,NC", [(2, 4, 4), (3, 8, 4), (1, 1, 1)])
+def test_dropped_signal_times_out_instead_of_hanging(models, P, NP, NC):
+    rc, out = run(models["PLANT_DROP_SIGNAL"], P, NP, NC, 2000, limit_ms=300)
+    assert rc == 2, out
+    assert "ThreadSanitizer" not in out, out
