@@ -35,6 +35,12 @@
  * epilogue stores only inside C.  They run the general variant of the
  * kernel, which always uses the register-staged producers.
  *
+ * Empty problems: M, N or K may be 0.  The configuration is still
+ * validated; no GEMM kernel is launched (plan grid 0).  With M or N = 0 a
+ * run does nothing; with K = 0 it writes C <- beta C (zeros for the default
+ * epilogue: the product of an empty sum).  Pointers the run does not use
+ * may be NULL: all three when M or N = 0, A and B when K = 0.
+ *
  * Ownership: A, B and C are device pointers owned by the caller.  A handle
  * owns its host-side plan and a small device word for the wait watchdog.
  *
@@ -52,7 +58,7 @@
 extern "C" {
 #endif
 
-#define WS_GEMM_ABI_VERSION 5
+#define WS_GEMM_ABI_VERSION 6
 
 typedef struct ws_gemm_handle* ws_gemm_t; /* opaque handle */
 
@@ -60,7 +66,7 @@ typedef enum { WS_F16 = 0, WS_BF16 = 1 } ws_dtype;
 
 typedef enum {
   WS_OK = 0,
-  WS_ERR_INVALID_ARG = 1,   /* NULL pointer, non-positive or oversized dimension, bad field */
+  WS_ERR_INVALID_ARG = 1,   /* NULL pointer, negative or oversized dimension, bad field */
   WS_ERR_UNSUPPORTED = 2,   /* valid request with no compiled kernel or wave arrangement */
   WS_ERR_LDS_OVERFLOW = 3,  /* stages x (A tile + B tile) does not fit in 160 KiB of LDS */
   WS_ERR_HIP = 4,           /* a HIP runtime call failed */
@@ -86,7 +92,7 @@ typedef struct {
 } ws_gemm_config;
 
 typedef struct {
-  int32_t grid;      /* persistent workgroups launched */
+  int32_t grid;      /* persistent workgroups launched; 0 for an empty problem (M, N or K = 0) */
   int32_t block;     /* threads per workgroup: 64 x (producer_waves + consumer_waves) */
   int32_t lds_bytes; /* LDS per workgroup: 256 + stages x 2 x (T_M T_K + T_K T_N) */
   int32_t tiles_m, tiles_n, tiles; /* output tiles per dimension and in total (Section 2.1) */
@@ -152,8 +158,9 @@ ws_status ws_gemm_create(int64_t M, int64_t N, int64_t K, const ws_gemm_config* 
 /* Enqueue C = A B (or the handle's epilogue) on `stream` (0 = the null
  * stream).  A (M x K) and B (K x N) must be 16-byte aligned device pointers,
  * C (M x N, element type of the epilogue's out_dtype) aligned to its element
- * size.  Does not synchronise.  Every element of C is written; nothing
- * outside it. */
+ * size; pointers an empty problem does not use may be NULL.  Does not
+ * synchronise.
+ * Every element of C is written; nothing outside it. */
 ws_status ws_gemm_run(ws_gemm_t h, const void* A, const void* B, void* C, hipStream_t stream);
 
 /* Synchronise `stream`, then report and clear the watchdog word:
@@ -208,7 +215,8 @@ ws_status ws_gemm_set_trace(ws_gemm_t h, void* buffer, int64_t bytes, int32_t wg
  * Run with ws_gemm_run (A, B, C as for the GEMM).  C is only written by
  * WS_CALIB_EPILOGUE (zeros); the other kinds leave it untouched.  Tracing is
  * not available on these handles.  WS_ERR_UNSUPPORTED when no calibration
- * variant of cfg was compiled. */
+ * variant of cfg was compiled, and for shapes the tiles do not divide or
+ * empty problems (no GEMM launch to calibrate). */
 typedef enum {
   WS_CALIB_NONE = -1, /* the GEMM itself (ws_gemm_create) */
   WS_CALIB_EMPTY = 0,

@@ -1263,6 +1263,16 @@ __device__ __forceinline__ void consumer_epilogue_only(const KernelArgs& args, i
   }
 }
 
+// The epilogue of a product with K = 0 (nothing to multiply): C <- beta C
+// over n elements of type T; zeros when beta == 0 (C is then not read).
+template <typename T>
+__global__ void __launch_bounds__(256) ws_scale_kernel(void* C, int64_t n, float beta) {
+  T* c = (T*)C;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+    c[i] = beta == 0.0f ? (T)0.0f : (T)(beta * load_out(c + i));
+}
+
 // Calibration of the launch itself (T_INIT): an empty kernel launched with
 // the GEMM's grid, block and LDS size.  A template so that every translation
 // unit including this header may instantiate it.

@@ -90,7 +90,7 @@ inline bool is_pow2_in(int x, int lo, int hi) {
 inline int plan_launch(const PlanIn& in, PlanOut* out) {
   if (!out) return kPlanInvalid;
   *out = PlanOut{};
-  if (in.M <= 0 || in.N <= 0 || in.K <= 0) return kPlanInvalid;
+  if (in.M < 0 || in.N < 0 || in.K < 0) return kPlanInvalid;
   if (in.M > (1 << 30) || in.N > (1 << 30) || in.K > (1 << 30)) return kPlanInvalid;
   if (in.dtype != 0 && in.dtype != 1) return kPlanInvalid;
   if (in.load_path != 0 && in.load_path != 1) return kPlanInvalid;
@@ -108,20 +108,32 @@ inline int plan_launch(const PlanIn& in, PlanOut* out) {
   if (wm < 32 || wn < 32 || wm * wn > (np == 0 ? 128 * 128 : 128 * 64)) return kPlanUnsupported;
   if (np == 0 ? (in.stages < 1 || in.stages > 2) : (in.stages < 2 || in.stages > kPlanMaxStages))
     return kPlanInvalid;
-  // The paper's model assumes whole tiles.  Other shapes run the ragged
-  // kernel variant (partial edge tiles, a partial last K-iteration), which
-  // needs 16-byte rows of A and B (K and N multiples of 8) and producer waves.
-  const bool ragged = (in.M % in.tile_m) || (in.N % in.tile_n) || (in.K % in.tile_k);
-  if (ragged && (in.K % 8 || in.N % 8 || np == 0)) return kPlanNotDivisible;
-  // element offsets inside one tile panel are 32-bit
-  // byte offsets inside one tile panel (A, B and the C epilogue) are 32-bit
-  if ((int64_t)in.tile_m * in.K * 2 >= (1ll << 31) || (int64_t)in.tile_k * in.N * 2 >= (1ll << 31) ||
-      (int64_t)in.tile_m * in.N * 4 >= (1ll << 31))
-    return kPlanInvalid;
   const int64_t stage = 2ll * (in.tile_m * in.tile_k + in.tile_k * in.tile_n);
   const int64_t lds = kPlanHeaderBytes + in.stages * stage;
   if (lds > kLdsLimit) return kPlanLdsOverflow;
   if (in.num_cus <= 0) return kPlanInvalid;
+  // An empty problem (M, N or K = 0) launches no GEMM kernel: grid 0.  With
+  // K = 0 and M N > 0, running it still writes C (the epilogue of a zero
+  // product).
+  if (in.M == 0 || in.N == 0 || in.K == 0) {
+    out->block = 64 * (nc + np);
+    out->lds_bytes = (int32_t)lds;
+    out->tiles_m = (int32_t)((in.M + in.tile_m - 1) / in.tile_m);
+    out->tiles_n = (int32_t)((in.N + in.tile_n - 1) / in.tile_n);
+    out->iters = (int32_t)((in.K + in.tile_k - 1) / in.tile_k);
+    out->split = np / nc;
+    out->group_m = 1;
+    return kPlanOk;
+  }
+  // The paper's model assumes whole tiles.  Other shapes run the general
+  // kernel variant (partial edge tiles, a partial last K-iteration), which
+  // needs 16-byte rows of A and B (K and N multiples of 8) and producer waves.
+  const bool ragged = (in.M % in.tile_m) || (in.N % in.tile_n) || (in.K % in.tile_k);
+  if (ragged && (in.K % 8 || in.N % 8 || np == 0)) return kPlanNotDivisible;
+  // byte offsets inside one tile panel (A, B and the C epilogue) are 32-bit
+  if ((int64_t)in.tile_m * in.K * 2 >= (1ll << 31) || (int64_t)in.tile_k * in.N * 2 >= (1ll << 31) ||
+      (int64_t)in.tile_m * in.N * 4 >= (1ll << 31))
+    return kPlanInvalid;
 
   const int64_t tm = (in.M + in.tile_m - 1) / in.tile_m, tn = (in.N + in.tile_n - 1) / in.tile_n;
   if (tm * tn >= (1ll << 31)) return kPlanInvalid;

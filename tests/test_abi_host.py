@@ -32,7 +32,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_text():
-    assert w.ws_gemm_abi_version() == 5
+    assert w.ws_gemm_abi_version() == 6
     for s in range(7):
         assert w.ws_gemm_status_str(s) and w.ws_gemm_status_str(s) != "unknown status"
     assert w.ws_gemm_status_str(99) == "unknown status"
@@ -77,8 +77,12 @@ def test_lds_overflow_case_from_the_sweep():
 @pytest.mark.parametrize("M,N,K,tile,status", [
     (8192, 8192, 8192 + 4, (256, 128, 64), w.WS_ERR_NOT_DIVISIBLE),   # ragged K not a multiple of 8
     (8192, 8192 + 12, 8192, (256, 128, 64), w.WS_ERR_NOT_DIVISIBLE),  # ragged N not a multiple of 8
-    (0, 8192, 8192, (256, 128, 64), w.WS_ERR_INVALID_ARG),
+    (-1, 8192, 8192, (256, 128, 64), w.WS_ERR_INVALID_ARG),
     (8192, -1, 8192, (256, 128, 64), w.WS_ERR_INVALID_ARG),
+    (8192, 8192, -8, (256, 128, 64), w.WS_ERR_INVALID_ARG),
+    (0, 8192, 8192, (48, 128, 64), w.WS_ERR_INVALID_ARG),           # empty, but a bad tile
+    (0, 8192, 8192, (256, 256, 32), w.WS_ERR_UNSUPPORTED),          # empty, unsupported waves
+    (8192, 8192, 0, (256, 128, 128), w.WS_ERR_LDS_OVERFLOW),        # empty, ring too large
     (8192, 8192, 8192, (48, 128, 64), w.WS_ERR_INVALID_ARG),
     (8192, 8192, 8192, (512, 128, 64), w.WS_ERR_INVALID_ARG),
     (8192, 8192, 8192, (256, 128, 16), w.WS_ERR_INVALID_ARG),
@@ -213,3 +217,21 @@ def test_plan_ragged_shapes(M, N, K):
     assert info.ragged == 0 and info.general == 0
     # the synchronous kernel takes whole tiles only
     assert w.ws_gemm_plan(M, N, K, cfg((tm, tn, tk), 2, 0, 4), 256, 1)[0] == w.WS_ERR_NOT_DIVISIBLE
+
+
+@pytest.mark.parametrize("M,N,K", [(0, 8192, 8192), (8192, 0, 8192), (8192, 8192, 0), (0, 0, 0), (5, 12, 0)])
+def test_plan_empty_problems(M, N, K):
+    """Empty problems plan no GEMM launch (grid 0); the configuration is
+    still validated, and shapes the tiles would not divide are accepted
+    (there is nothing to tile)."""
+    tm, tn, tk = 256, 128, 64
+    s, info = w.ws_gemm_plan(M, N, K, cfg((tm, tn, tk)), 256, 1)
+    assert s == w.WS_OK, w.ws_gemm_status_str(s)
+    assert info.grid == 0 and info.tiles == 0 and info.rounds == 0 and info.ragged == 0
+    assert info.tiles_m == -(-M // tm) and info.tiles_n == -(-N // tn) and info.iters == -(-K // tk)
+    assert info.block == 512 and info.lds_bytes == 256 + 3 * 2 * (tm * tk + tk * tn)
+    # no tile to schedule
+    assert w.ws_gemm_schedule(info, 0, 0)[0] == w.WS_ERR_INVALID_ARG
+    # the synchronous kernel's configurations plan empty problems too
+    assert w.ws_gemm_plan(M, N, K, cfg((tm, tn, tk), 2, 0, 4), 256, 1)[0] == w.WS_OK
+
