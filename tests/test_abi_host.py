@@ -235,3 +235,21 @@ def test_plan_empty_problems(M, N, K):
     # the synchronous kernel's configurations plan empty problems too
     assert w.ws_gemm_plan(M, N, K, cfg((tm, tn, tk), 2, 0, 4), 256, 1)[0] == w.WS_OK
 
+
+
+@pytest.mark.parametrize("M,N,K,status", [
+    (8192, 8192, (1 << 31) // (2 * 256), w.WS_ERR_INVALID_ARG),        # 256 K 2 bytes of an A panel reach 2^31
+    (8192, 8192, (1 << 31) // (2 * 256) - 64, w.WS_OK),
+    (8192, (1 << 31) // (4 * 256), 8192, w.WS_ERR_INVALID_ARG),        # 256 N 4 bytes of a C panel reach 2^31
+    (8192, (1 << 31) // (4 * 256) - 128, 8192, w.WS_OK),
+    ((1 << 30) + 1, 128, 64, w.WS_ERR_INVALID_ARG),                    # dimensions are capped at 2^30
+    (1 << 30, 128, 64, w.WS_OK),
+    (1 << 30, 1 << 20, 64, w.WS_ERR_INVALID_ARG),                      # 2^31 output tiles
+])
+def test_plan_size_limits(M, N, K, status):
+    """The largest accepted problems: byte offsets inside one tile panel are
+    32-bit, so T_M K 2, T_K N 2 and T_M N 4 must stay below 2^31."""
+    s, info = w.ws_gemm_plan(M, N, K, cfg((256, 128, 64)), 256, 1)
+    assert s == status, w.ws_gemm_status_str(s)
+    if s == w.WS_OK:
+        assert info.tiles == -(-M // 256) * -(-N // 128) and info.iters == -(-K // 64)
