@@ -7,8 +7,12 @@ C = A B.  Operands are generated once (seeded, synthetic) and are resident in
 HBM before the timed region starts.
 
     python bench.py [--gpus 1] [--steps 100] [--warmup 50] [--point TMxTNxTKxSxNPxNC]
+                    [--workload NAME]
 
-Prints one JSON line.  Also reported: the dominant kernel's roofline entry
+Prints one JSON line.  The default workload is the 8192^3 product above;
+--workload runs another of the GEMM workloads (paper_2506_11209_amd/
+workloads.py) at its own launch point, with the roofline taken against HBM
+bandwidth when its arithmetic intensity is below the ridge point.  Also reported: the dominant kernel's roofline entry
 (device time per launch from HIP events on the launch stream) and the CPU
 oracle timed on this host's cores over a bounded sample of the same product.
 """
@@ -26,7 +30,8 @@ sys.path.insert(0, ROOT)
 WORKLOAD = "gemm_8192x8192x8192_bf16_normal"
 DEFAULT_POINT = (256, 128, 64, 3, 4, 4)   # (TM, TN, TK, stages, producer waves, consumer waves)
 DEFAULT_LOAD_PATH = "registers"
-PEAK_TFLOPS = 2500.0                      # MI355X dense bf16 MFMA
+PEAK_TFLOPS = 2500.0                      # MI355X dense bf16 / fp16 MFMA
+PEAK_HBM_GBS = 8000.0                     # MI355X HBM3E
 PROFILES = os.path.join(ROOT, "profiles")
 
 
@@ -38,19 +43,20 @@ def kernel_fingerprint(point=DEFAULT_POINT, dtype="bf16") -> str:
     return code_fingerprint(gemm_symbol(tm, tn, tk, nc, np_ // nc, bf16=(dtype == "bf16")))
 
 
-def traffic_for(point_key: str, point=DEFAULT_POINT):
+def traffic_for(point_key: str, point=DEFAULT_POINT, dtype="bf16", workload=WORKLOAD):
     """HBM bytes per launch from the committed counter runs (profiles/
-    *hbm_traffic*.json), if they were taken on this launch point and on the
-    machine code the library now holds for it; else None."""
+    *hbm_traffic*.json), if they were taken on this workload and launch point
+    and on the machine code the library now holds for it; else None."""
     import glob
-    fp = kernel_fingerprint(point)
+    fp = kernel_fingerprint(point, dtype)
     for path in sorted(glob.glob(os.path.join(PROFILES, "*hbm_traffic*.json"))):
         try:
             with open(path) as f:
                 t = json.load(f)
         except (OSError, ValueError):
             continue
-        if t.get("kernel_fingerprint") == fp and t.get("point") == point_key:
+        if (t.get("kernel_fingerprint") == fp and t.get("point") == point_key
+                and t.get("workload") == workload):
             return t.get("traffic_bytes_per_launch")
     return None
 
@@ -89,6 +95,7 @@ def main():
     ap.add_argument("--point", default=None, help="TMxTNxTKxSTAGESxNPxNC")
     ap.add_argument("--load-path", default=DEFAULT_LOAD_PATH, choices=("registers", "dma"))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", default=WORKLOAD)
     a = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if a.gpus != 1 or world != 1:
@@ -105,8 +112,14 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
-    wl = WORKLOADS[WORKLOAD]
-    point = tuple(int(x) for x in a.point.split("x")) if a.point else DEFAULT_POINT
+    if a.workload not in WORKLOADS:
+        print("unknown workload %s; one of %s" % (a.workload, sorted(WORKLOADS)), file=sys.stderr)
+        sys.exit(2)
+    wl = WORKLOADS[a.workload]
+    if a.point:
+        point = tuple(int(x) for x in a.point.split("x"))
+    else:
+        point = DEFAULT_POINT if wl.name == WORKLOAD else wl.points[0]
     tm, tn, tk, stages, np_, nc = point
     A, B = inputs.make_operands(wl.M, wl.N, wl.K, wl.dtype, wl.dist, wl.seed)
     Ad, Bd = A.cuda(), B.cuda()
@@ -126,10 +139,20 @@ def main():
         sys.exit(1)
     sm = summary(dev)
     value = wl.flops / (wall_ms * 1e-3) / 1e12
-    achieved = wl.flops / (sm["mean_ms"] * 1e-3) / 1e12
     pkey = "x".join(map(str, point)) + "/" + a.load_path
+    # roofline of the kernel: MFMA peak, or HBM bandwidth below the ridge point
+    if wl.flops / wl.bytes >= PEAK_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
+        bound, unit, peak = "mfma", "TFLOP/s", PEAK_TFLOPS
+        achieved = wl.flops / (sm["mean_ms"] * 1e-3) / 1e12
+    else:
+        bound, unit, peak = "hbm", "GB/s", PEAK_HBM_GBS
+        achieved = wl.bytes / (sm["mean_ms"] * 1e-3) / 1e9
+    if wl.name == WORKLOAD:
+        metric = "bf16 GEMM TFLOP/s at 8192^3 (fraction of dense MFMA peak in pct_mfma_peak)"
+    else:
+        metric = "%s GEMM TFLOP/s at %dx%dx%d" % (wl.dtype, wl.M, wl.N, wl.K)
     out = {
-        "metric": "bf16 GEMM TFLOP/s at 8192^3 (fraction of dense MFMA peak in pct_mfma_peak)",
+        "metric": metric,
         "value": round(value, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -139,17 +162,19 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": wl.dtype,
         "data": "synthetic",
         "pct_mfma_peak": round(100.0 * value / PEAK_TFLOPS, 2),
         "config": {"workload": wl.name, "M": wl.M, "N": wl.N, "K": wl.K,
                    "tile": [tm, tn, tk], "stages": stages, "producer_waves": np_,
                    "consumer_waves": nc, "split": "%d:1" % (np_ // nc),
                    "load_path": a.load_path, "grid": g.info.grid, "rounds": g.info.rounds},
-        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS, 4),
-                     "traffic": traffic_for(pkey, point),
-                     "kernel": "ws_gemm_kernel<%d,%d,%d,%d,%d,bf16>" % (tm, tn, tk, nc, np_ // nc),
+        "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak,
+                     "unit": unit, "frac": round(achieved / peak, 4),
+                     "traffic": traffic_for(pkey, point, wl.dtype, wl.name) if np_ > 0 else None,
+                     "kernel": ("ws_gemm_kernel<%d,%d,%d,%d,%d,%s>" % (tm, tn, tk, nc, np_ // nc, wl.dtype)
+                                if np_ > 0 else "ws_sync_kernel<%d,%d,%d,%d,%s>" % (tm, tn, tk, nc, wl.dtype)),
+                     "algorithmic_bytes": wl.bytes, "flop": wl.flops,
                      "launch_ms": {k: round(v, 5) if isinstance(v, float) else v for k, v in sm.items()}},
     }
     g.close()

@@ -3,7 +3,7 @@
     python -m paper_2506_11209_amd.profsummary trace  DB [--kernel SUBSTR] [--skip N]
     python -m paper_2506_11209_amd.profsummary counters DB [--kernel SUBSTR]
     python -m paper_2506_11209_amd.profsummary traffic FETCH_DB WRITE_DB CAL_FETCH_DB CAL_WRITE_DB \
-        --kernel SUBSTR --point KEY [--copy-mib 1024]
+        --kernel SUBSTR --point KEY [--workload NAME] [--dtype bf16] [--copy-mib 1024]
 
 `trace`: per-kernel call count, mean / median / min duration (us), from
 `rocprofv3 --kernel-trace` (with `--group G`: the matching dispatches in
@@ -66,19 +66,20 @@ def _mean_counter(db_path, name_part, counter):
     return vals[0]
 
 
-def traffic(fetch_db, write_db, cal_fetch_db, cal_write_db, kernel, point, copy_mib):
+def traffic(fetch_db, write_db, cal_fetch_db, cal_write_db, kernel, point, copy_mib, workload, dtype):
     import json
     import os
     import sys
     sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
-    from bench import kernel_fingerprint
+    from bench import WORKLOAD, kernel_fingerprint
     point_t = tuple(int(x) for x in point.split("/")[0].split("x"))
     copy_bytes = copy_mib * (1 << 20)
     f_scale = copy_bytes / (_mean_counter(cal_fetch_db, "copyBuffer", "FETCH_SIZE") * 1024)
     w_scale = copy_bytes / (_mean_counter(cal_write_db, "copyBuffer", "WRITE_SIZE") * 1024)
     fetch = _mean_counter(fetch_db, kernel, "FETCH_SIZE")
     write = _mean_counter(write_db, kernel, "WRITE_SIZE")
-    rec = {"kernel": kernel, "point": point, "kernel_fingerprint": kernel_fingerprint(point_t),
+    rec = {"kernel": kernel, "workload": workload or WORKLOAD, "point": point,
+           "kernel_fingerprint": kernel_fingerprint(point_t, dtype),
            "fetch_size_kib": fetch, "write_size_kib": write,
            "fetch_scale_bytes_per_kib": f_scale * 1024, "write_scale_bytes_per_kib": w_scale * 1024,
            "traffic_bytes_per_launch": fetch * 1024 * f_scale + write * 1024 * w_scale}
@@ -92,11 +93,13 @@ def main(argv=None):
     ap.add_argument("--kernel", default=None)
     ap.add_argument("--point", default=None)
     ap.add_argument("--copy-mib", type=int, default=1024)
+    ap.add_argument("--workload", default=None, help="traffic: workload the counters ran (default: the bench's)")
+    ap.add_argument("--dtype", default="bf16", help="traffic: operand dtype of the kernel")
     ap.add_argument("--skip", type=int, default=0, help="trace: leading dispatches per kernel (or run) to drop")
     ap.add_argument("--group", type=int, default=0, help="trace: dispatches per consecutive run")
     a = ap.parse_args(argv)
     if a.mode == "traffic":
-        traffic(*a.db[:4], a.kernel, a.point, a.copy_mib)
+        traffic(*a.db[:4], a.kernel, a.point, a.copy_mib, a.workload, a.dtype)
         return
     a.db = a.db[0]
     if a.mode == "trace" and a.group > 0:

@@ -39,11 +39,12 @@ def test_traffic_record_matches_only_its_own_kernel(tmp_path, monkeypatch):
     import bench
     point = (256, 128, 64, 3, 4, 4)
     rec = {"point": "256x128x64x3x4x4/registers", "kernel_fingerprint": bench.kernel_fingerprint(point),
-           "traffic_bytes_per_launch": 123.0}
+           "workload": bench.WORKLOAD, "traffic_bytes_per_launch": 123.0}
     (tmp_path / "x_hbm_traffic.json").write_text(json.dumps(rec))
     monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
     assert bench.traffic_for("256x128x64x3x4x4/registers", point) == 123.0
     assert bench.traffic_for("256x128x64x3x4x4/dma", point) is None
+    assert bench.traffic_for("256x128x64x3x4x4/registers", point, workload="gemm_4096x4096x4096_bf16_normal") is None
     rec["kernel_fingerprint"] = "0" * 16
     (tmp_path / "x_hbm_traffic.json").write_text(json.dumps(rec))
     assert bench.traffic_for("256x128x64x3x4x4/registers", point) is None
