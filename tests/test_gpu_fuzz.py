@@ -73,3 +73,36 @@ def test_random_case_is_exact(i):
     ref = E.epilogue(AB, C_in.to(torch.float64).numpy(), alpha, beta, out)
     r = compare_exact(res[:M * N].reshape(M, N), ref)
     assert r["ok"], (c, r)
+
+
+SYNC_CONFIGS = sorted({(tm, tn, tk, nc, bf16)
+                       for (tm, tn, tk, nc, split, bf16, trace, mode, general) in instances() if split == 0})
+N_SYNC_CASES = 2 * len(SYNC_CONFIGS)
+
+
+@pytest.mark.parametrize("i", range(N_SYNC_CASES))
+def test_random_synchronous_case_is_exact(i):
+    """The synchronous kernel (no producer waves) takes whole tiles and the
+    default epilogue: random multiples of each compiled tile, ring depth 1
+    or 2 where it fits."""
+    rng = np.random.default_rng(9000 + i)
+    tm, tn, tk, nc, bf16 = SYNC_CONFIGS[i % len(SYNC_CONFIGS)]
+    dtype = "bf16" if bf16 else "f16"
+    M, N, K = (int(rng.integers(1, 4)) * tm, int(rng.integers(1, 4)) * tn, int(rng.integers(1, 6)) * tk)
+    fits2 = 256 + 2 * 2 * (tm * tk + tk * tn) <= 163840
+    stages = int(rng.integers(1, 3)) if fits2 else 1
+    log("case fuzz sync %d %dx%dx%d tile=%s nc=%d P=%d %s" % (i, M, N, K, (tm, tn, tk), nc, stages, dtype))
+    A, B = inputs.make_operands(M, N, K, dtype, "int4", 9500 + i)
+    g = w.WsGemm(M, N, K, (tm, tn, tk), stages, 0, nc, dtype)
+    try:
+        buf = torch.full((M * N + GUARD,), SENTINEL, device="cuda")
+        Ad, Bd = A.cuda(), B.cuda()
+        g.run_ptrs(Ad.data_ptr(), Bd.data_ptr(), buf.data_ptr(), torch.cuda.current_stream().cuda_stream)
+        assert g.sync_status() == w.WS_OK
+        res = buf.cpu().numpy()
+    finally:
+        g.close()
+    assert np.all(res[M * N:] == SENTINEL)
+    AB, _ = oracle.gemm(inputs.bits(A), inputs.bits(B), dtype, with_abs=False)
+    r = compare_exact(res[:M * N].reshape(M, N), AB)
+    assert r["ok"], r
