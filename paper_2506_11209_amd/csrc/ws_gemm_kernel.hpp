@@ -1,6 +1,8 @@
 // Warp-specialised tiled GEMM kernel for gfx950 (MI355X).
 //
-// C (M x N, fp32) = A (M x K) * B (K x N), A and B fp16 or bf16, all row-major.
+// C (M x N, fp32) = A (M x K) * B (K x N), A and B fp16 or bf16, all row-major
+// (the general variant below also stores alpha A B + beta C as fp32, bf16 or
+// fp16, and handles partial edge tiles).
 // The kernel follows the producer/consumer structure of the GeMM-WS kernel the
 // paper models (Section 1.3, Algorithm 1): inside each workgroup, producer
 // ("DMA") wavefronts move A and B tiles from global memory into a circular
@@ -15,10 +17,12 @@
 //    (Section 1.2).  Waves [0, NC) are consumers, waves [NC, NC + NP) are
 //    producers.  With NC = 4 the consumers sit one per SIMD and tile the
 //    output block 2 x 2.
-//  * Producers use global_load_lds_dwordx4: 64 lanes x 16 bytes go straight
-//    from memory into 1 KiB of LDS without passing through VGPRs.  The LDS
-//    placement of every 16-byte chunk is chosen through the global address
-//    each lane fetches.
+//  * Producers move a tile in 16-byte chunks, 1 KiB per wave instruction,
+//    either staged through VGPRs several K-iterations ahead
+//    (global_load_dwordx4, then ds_write_b128 once the slot is free; the
+//    default) or with global_load_lds_dwordx4 straight into the slot.  The
+//    LDS placement of every chunk is fixed by the lane; the layout below is
+//    produced by choosing which global chunk each lane fetches.
 //  * 1:1 split (NP == NC): every producer loads a share of the A tile and then
 //    a share of the B tile, in that order (one DMA warp loading both tiles).
 //    2:1 split (NP == 2 NC): the first half of the producers loads A, the
@@ -31,6 +35,10 @@
 //    places the tiles that run at the same time on one XCD next to each
 //    other so that they share A row panels and B column panels in that XCD's
 //    L2.
+//  * Variants of one template: the plain GEMM, its event-traced twin, the
+//    calibration kernels of the performance model (KernelMode), and the
+//    general variant (GENERAL: partial tiles and the alpha / beta epilogue).
+//    Slot and counter arithmetic is in ws_ring.hpp.
 //
 // LDS layout (dynamic shared memory)
 //   [0, 256)            counters: full[8], empty[8], abort
