@@ -5,7 +5,10 @@ depths and producer/consumer wave splits on one GPU.
         [--steps 30] [--warmup 5] [--out sweep.jsonl]
 
 One JSON line per launch point: device time (mean/median/std over HIP-event
-pairs), TFLOP/s, fraction of the dense MFMA peak and of the HBM roofline.
+pairs), TFLOP/s, fraction of the dense MFMA peak and of the HBM roofline, and
+the largest error on 16 sampled rows of C against a float32 torch product,
+scaled by |A||B| (a sanity figure; the parity tests check against the CPU
+oracle).
 Points whose ring does not fit in LDS are reported with their status.
 Appends to --out and skips points already present there, so an interrupted
 sweep resumes.
@@ -62,10 +65,16 @@ def measure_point(wl, point, Ad, Bd, C, steps, warmup, load_path="registers"):
     sm = summary(dev)
     t = sm["mean_ms"] * 1e-3
     tflops = wl.flops / t / 1e12
+    rows = torch.linspace(0, wl.M - 1, 16, device=Ad.device).long()
+    Ar, Bf = Ad[rows].float(), Bd.float()
+    scale = (Ar.abs() @ Bf.abs()).clamp_min(torch.finfo(torch.float32).tiny)
+    max_scaled_err = float(((C[rows] - Ar @ Bf).abs() / scale).max())
+    del Bf
     rec.update({
         "status": "ok", "plan": info.as_dict(), "device_ms": sm, "wall_ms_per_launch": wall,
         "tflops": tflops, "frac_mfma_peak": tflops / PEAK_TFLOPS[wl.dtype],
         "hbm_gbs_algorithmic": wl.bytes / t / 1e9, "frac_hbm_roofline": wl.bytes / t / 1e9 / PEAK_HBM_GBS,
+        "max_scaled_err": max_scaled_err,
     })
     return rec
 
