@@ -5,7 +5,7 @@
 For each producer arrangement (one DMA wave group loading A then B, and two
 loading A and B concurrently) and load path, with the calibration kernels of
 the library (``ws_gemm_create_calibration``) on the launch of an 8192 x 8192
-output (full grid, several rounds):
+output (full grid, several rounds; --mn sets another square output):
 
   T_INIT      the empty kernel's time;
   T_EPILOGUE  (epilogue-only kernel time - T_INIT) / rounds;
@@ -24,7 +24,8 @@ B loads cost the same per element).
 With --table, T_MATH, T_LOAD-A, T_LOAD-B and the time of loading both tiles
 (the producers' own rate, WS_CALIB_LOAD_AB) are also measured directly for
 every tile of the accuracy grid (model_eval.py), so that the event model can
-be evaluated apart from the linear cost model.  Writes one JSON document
+be evaluated apart from the linear cost model; --table-tiles paper measures
+the tiles of the paper's own grid instead.  Writes one JSON document
 with every raw measurement.
 """
 from __future__ import annotations
@@ -44,8 +45,11 @@ from paper_2506_11209_amd.timing import time_launches
 MN = 8192
 K_PAIR = (1024, 4096)
 PAIRS = {1: ((128, 128, 64), (256, 128, 64)), 2: ((128, 128, 64), (128, 128, 32))}
-TABLE_TILES = ((128, 128, 64), (256, 128, 64), (128, 256, 64), (64, 64, 64), (128, 128, 32),
-               (128, 256, 32))
+TABLE_TILES = {
+    "accuracy": ((128, 128, 64), (256, 128, 64), (128, 256, 64), (64, 64, 64), (128, 128, 32),
+                 (128, 256, 32)),
+    "paper": ((64, 64, 64), (64, 128, 64), (128, 64, 64), (128, 128, 64)),
+}
 LDS_LIMIT = 163840
 
 
@@ -75,9 +79,10 @@ def kernel_us(kind, M, N, K, tile, np_, load_path, A, B, C, steps, warmup):
 def per_iteration_us(kind, tile, np_, load_path, bufs, steps, warmup):
     """Time one workgroup spends per K-iteration, from two values of K."""
     A, B, C = bufs
+    mn = C.shape[0]
     tk = tile[2]
-    t1, W = kernel_us(kind, MN, MN, K_PAIR[0], tile, np_, load_path, A, B, C, steps, warmup)
-    t2, _ = kernel_us(kind, MN, MN, K_PAIR[1], tile, np_, load_path, A, B, C, steps, warmup)
+    t1, W = kernel_us(kind, mn, mn, K_PAIR[0], tile, np_, load_path, A, B, C, steps, warmup)
+    t2, _ = kernel_us(kind, mn, mn, K_PAIR[1], tile, np_, load_path, A, B, C, steps, warmup)
     iters = W * (K_PAIR[1] - K_PAIR[0]) // tk
     return (t2 - t1) / iters, {"t_k1_us": t1, "t_k2_us": t2, "rounds": W}
 
@@ -91,11 +96,13 @@ def costs(tile, np_, load_path, bufs, steps, warmup):
 
 
 def calibrate(split, load_path, bufs, steps, warmup, table):
+    """table: None, or the tiles to measure one by one."""
     np_ = 4 * split
     A, B, C = bufs
+    mn = C.shape[0]
     tile0 = PAIRS[split][0]
-    t_init, _ = kernel_us("empty", MN, MN, K_PAIR[0], tile0, np_, load_path, A, B, C, steps, warmup)
-    t_epi_kernel, W = kernel_us("epilogue", MN, MN, tile0[2], tile0, np_, load_path, A, B, C, steps,
+    t_init, _ = kernel_us("empty", mn, mn, K_PAIR[0], tile0, np_, load_path, A, B, C, steps, warmup)
+    t_epi_kernel, W = kernel_us("epilogue", mn, mn, tile0[2], tile0, np_, load_path, A, B, C, steps,
                                 warmup)
     t_epi = (t_epi_kernel - t_init) / W
     raw = {"t_init_us": t_init, "epilogue_kernel_us": t_epi_kernel, "epilogue_rounds": W}
@@ -117,7 +124,7 @@ def calibrate(split, load_path, bufs, steps, warmup, table):
            "load_a": loads, "load_b": loads_b, "math": maths}
     if table:
         rows = []
-        for tile in TABLE_TILES:
+        for tile in table:
             (la, _), (lb, _), (mm, _) = costs(tile, np_, load_path, bufs, steps, warmup)
             lab, _ = per_iteration_us("load_ab", tile, np_, load_path, bufs, steps, warmup)
             rows.append({"tile": tile, "stages": stages_for(tile), "t_load_a": la, "t_load_b": lb,
@@ -134,24 +141,27 @@ def main(argv=None):
     ap.add_argument("--splits", default="1,2")
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--table", action="store_true", help="also measure every tile of the accuracy grid")
+    ap.add_argument("--table", action="store_true", help="also measure every tile of the evaluation grid")
+    ap.add_argument("--table-tiles", default="accuracy", choices=tuple(TABLE_TILES))
+    ap.add_argument("--mn", type=int, default=MN, help="rows and columns of the calibration output")
     ap.add_argument("--out", default=None)
     a = ap.parse_args(argv)
     torch.manual_seed(0)
-    A = torch.randn(MN, K_PAIR[1], device="cuda").to(torch.bfloat16)
-    B = torch.randn(K_PAIR[1], MN, device="cuda").to(torch.bfloat16)
-    C = torch.empty(MN, MN, device="cuda")
+    mn = a.mn
+    A = torch.randn(mn, K_PAIR[1], device="cuda").to(torch.bfloat16)
+    B = torch.randn(K_PAIR[1], mn, device="cuda").to(torch.bfloat16)
+    C = torch.empty(mn, mn, device="cuda")
     bufs = (A, B, C)
     # warm the clock up before the first measurement
-    g = w.WsGemm(MN, MN, K_PAIR[1], (256, 128, 64), 3, 4, 4, "bf16")
+    g = w.WsGemm(mn, mn, K_PAIR[1], (256, 128, 64), 3, 4, 4, "bf16")
     time_launches(lambda: g(A, B, C), 1, 50)
     g.close()
     out = {"device": torch.cuda.get_device_name(0), "time": time.strftime("%Y-%m-%d %H:%M:%S"),
-           "problem": {"M": MN, "N": MN, "K_pair": K_PAIR, "pairs": {str(k): v for k, v in PAIRS.items()}},
+           "problem": {"M": mn, "N": mn, "K_pair": K_PAIR, "pairs": {str(k): v for k, v in PAIRS.items()}},
            "calibrations": []}
     for lp in a.load_paths.split(","):
         for split in (int(x) for x in a.splits.split(",")):
-            rec = calibrate(split, lp, bufs, a.steps, a.warmup, a.table)
+            rec = calibrate(split, lp, bufs, a.steps, a.warmup, TABLE_TILES[a.table_tiles] if a.table else None)
             out["calibrations"].append(rec)
             log("split %d %s: %s" % (split, lp, json.dumps(rec["params"])))
     text = json.dumps(out, indent=1)
