@@ -29,7 +29,12 @@
 //    second half loads B, concurrently (two DMA warps, one tile each).
 //  * Consumers read operands with ds_read_b128 (A, K-contiguous) and
 //    ds_read_b64_tr_b16 (B, N-contiguous, transposed by the read) and
-//    accumulate with v_mfma_f32_32x32x16_{bf16,f16} in fp32.
+//    accumulate with v_mfma_f32_32x32x16_{bf16,f16} in fp32.  With TK = 64,
+//    one producer group and the 128x128, 128x256 and 256x128 tiles, the K
+//    loop of a tile is a generated asm block (consumer_deep,
+//    ws_deep_loop.inc) that keeps the reads of the next k-steps in flight
+//    behind the MFMAs; the other shapes, the event-traced twin and the
+//    register-lean 2:1 variants run compiler-scheduled consumers.
 //  * The grid is persistent: at most one workgroup per CU slot, each walking
 //    output tiles in dispatch rounds (Section 2.1, "Wave").  The tile order
 //    places the tiles that run at the same time on one XCD next to each
@@ -1085,6 +1090,96 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
 }
 
 // ---------------------------------------------------------------------------
+// Deep-prefetch consumer (four k-steps per K-iteration): the operands of
+// k-step t are read during k-step t - 3, so three k-steps of LDS reads stay in
+// flight behind the MFMAs.  The K loop of a tile is one generated asm block
+// (DeepLoop, ws_deep_loop.inc): its fragment registers are fixed and every
+// wait on an LDS read is placed by hand.  A wave's LDS operations complete in
+// order, so a wait names how many younger LDS operations may still be
+// outstanding.
+//
+// One K-iteration q that is not the last of its tile, in issue order (R_s(q)
+// = the reads of k-step s of q's slot, R = BM + 2 BN instructions):
+//   k-step 0  wait for R_0(q) (2R or more younger);  issue R_3(q);  MFMAs
+//   k-step 1  wait for R_1(q) and the counter peeked at k-step 2 of q - 1
+//             (2R younger); check q + 1's slot is full, polling (and
+//             draining every read) only when it is not; issue R_0(q + 1);
+//             MFMAs
+//   k-step 2  wait for R_2(q) (2R younger);  issue R_1(q + 1);  MFMAs;
+//             release q's slot once R_3(q) has completed (2R younger);
+//             peek at the full counter of q + 2
+//   k-step 3  wait for R_3(q) (2R + 2 younger);  issue R_2(q + 1);  MFMAs
+// Waits cap at 15, the counter's range: a wait for fewer outstanding
+// operations than needed only waits longer.  The last K-iteration of a tile
+// reads nothing ahead and drains (R younger at k-step 2, none at k-step 3);
+// the epilogue follows, and the next tile starts with a prologue: wait for
+// its first slot, issue R_0, R_1, the peek at the following slot (when the
+// tile has a second K-iteration) and R_2.
+// ---------------------------------------------------------------------------
+#include "ws_deep_loop.inc"
+
+template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, int MODE, bool GENERAL>
+__device__ __forceinline__ void consumer_deep(const KernelArgs& args, WSG_LDS char* smem, int cw,
+                                              int lane) {
+  using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
+  using Loop = DeepLoop<TM, TN, TK, NC, SPLIT, BF16>;
+  static_assert(Loop::kAvailable && G::KS == 4, "deep consumer configuration");
+  constexpr int BM = G::BM, BN = G::BN;
+  WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
+  WSG_LDS uint32_t* empty = full + kMaxStages;
+  WSG_LDS uint32_t* abort_flag = full + 2 * kMaxStages;
+
+  const int wm = cw / G::WGN, wn = cw % G::WGN;
+  // A operand of k-step s: row r, 16-byte chunk (2 s + lane / 32) ^ swz(r).
+  // Slots start on 128-byte boundaries, so the address for k-step s is the
+  // k-step 0 address with bits 5 and 6 XORed by 32 s.
+  const int r = wm * G::WM + (lane & 31);
+  const uint32_t a_off0 = (uint32_t)(r * TK * 2 + (((lane >> 5) ^ swz_a<TK>(r)) << 4));
+  // B operand: the k-step's 4 x 16 blocks, as in ConsumerOps::load_b, past the A tile.
+  const int grp = lane >> 4;
+  const uint32_t b_off = (uint32_t)(G::A_BYTES +
+                                    ((2 * (grp >> 1)) * G::NQ + (wn * G::WN) / 16 + (grp & 1)) * 128 +
+                                    8 * (lane & 15));
+  static_assert(kHeaderBytes % 128 == 0 && G::STAGE % 128 == 0, "slots on 128-byte boundaries");
+
+  const int Gd = gridDim.x;
+  const int g0 = first_slot(args);
+  if (g0 >= args.num_tiles) return;
+  const int my_tiles = (args.num_tiles - g0 + Gd - 1) / Gd;
+  const uint32_t S = (uint32_t)args.iters;
+  const uint32_t P = (uint32_t)args.stages;
+  const uint32_t ring = (uint32_t)(uintptr_t)(smem + kHeaderBytes);
+  const uint32_t fullb = (uint32_t)(uintptr_t)full;
+  const uint32_t emptyb = (uint32_t)(uintptr_t)empty;
+  const uint32_t abortb = (uint32_t)(uintptr_t)abort_flag;
+
+  int v = g0, ti, tj;
+  tile_coords(v, args.tiles_m, args.tiles_n, args.group_m, &ti, &tj);
+  f32x16_t acc[BM][BN];
+  uint32_t slot = 0, ftarget = (uint32_t)G::NP;  // K-iteration 0: ring_slot 0, ring_full_target NP
+  for (int t = 0; t < my_tiles; ++t) {
+#pragma unroll
+    for (int mb = 0; mb < BM; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < BN; ++nb) acc[mb][nb] = f32x16_t{};
+    if (!wait_counter(&full[slot], ftarget, abort_flag, args.spin_limit, args.err)) return;
+    const uint32_t st = Loop::tile(acc, a_off0, b_off, slot, ftarget, P, S, ring, fullb, emptyb, abortb,
+                                   args.spin_limit, args.consumer_delay);
+    if (st != 0) {
+      if (st == 2) report_timeout(abort_flag, args.err);
+      return;
+    }
+    // The calibration MATH kernel keeps its products (the store below is
+    // never taken: M > 0) without writing C.
+    if (MODE != kModeMath || args.M < 0)
+      store_tile<TM, TN, G::WM, G::WN, BM, BN, GENERAL, (BN > 2 ? 32 / BN : 16)>(args, acc, ti, tj, wm, wn,
+                                                                                  lane);
+    v += Gd;
+    tile_coords(v, args.tiles_m, args.tiles_n, args.group_m, &ti, &tj);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Register-lean consumer for three waves per SIMD (two producers per consumer
 // with the largest wave tiles): every operand fragment is single-buffered and
 // refilled right after its last MFMA of the k-step, and the loop body is one
@@ -1305,6 +1400,11 @@ __global__ void __launch_bounds__((NC + NC * SPLIT) * 64) ws_gemm_kernel(KernelA
       // Three waves per SIMD leave 168 VGPRs: the largest wave tiles then
       // take the single-buffered consumer.
       consumer_rolling<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
+    } else if constexpr (!TRACE && (MODE == kModeGemm || MODE == kModeMath) &&
+                         DeepLoop<TM, TN, TK, NC, SPLIT, BF16>::kAvailable) {
+      // TK = 64 with one producer group and the three largest tiles: the
+      // hand-scheduled deep-prefetch K loop.
+      consumer_deep<TM, TN, TK, NC, SPLIT, BF16, MODE, GENERAL>(args, smem, wave, lane);
     } else {
       consumer<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
     }

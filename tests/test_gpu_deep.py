@@ -1,0 +1,116 @@
+"""The deep-prefetch consumer (generated asm K loop, ws_deep_loop.inc) in every
+configuration that runs it (TK = 64, 4 + 4 waves, 128x128, 128x256 and
+256x128 tiles): its prologue, steady and last K-iterations (1, 2, 3 and 7
+K-iterations per tile), slot wrap-around at every ring depth that fits, two
+output tiles per workgroup, both producer load paths, the general variant,
+the polling path (late producers), the consumer delay hook and the watchdog.
+
+Operands are small integers, so every product is exact: C is compared with
+the oracle on sampled rows and, over all of C, by an exact checksum
+C x == A (B x) for a random +-1 vector x (fp64, integer-valued sums)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.check import compare_exact
+from paper_2506_11209_amd import inputs
+from tests.gpu_helpers import log, sample_rows
+
+w = pytest.importorskip("paper_2506_11209_amd.wsgemm")
+
+pytestmark = pytest.mark.gpu
+
+LDS_LIMIT = 163840
+TILES = [(256, 128, 64), (128, 256, 64), (128, 128, 64)]
+
+
+def max_stages(tile):
+    tm, tn, tk = tile
+    return (LDS_LIMIT - 256) // (2 * (tm * tk + tk * tn))
+
+
+def exact_checksum(C, A, B, seed):
+    rng = np.random.default_rng(seed)
+    x = rng.choice([-1.0, 1.0], size=C.shape[1])
+    Af = A.to(torch.float64).numpy()
+    Bf = B.to(torch.float64).numpy()
+    return np.array_equal(C.astype(np.float64) @ x, Af @ (Bf @ x))
+
+
+def run_and_check(M, N, K, tile, stages, dtype="bf16", load_path="registers", debug=None, seed=0):
+    A, B = inputs.make_operands(M, N, K, dtype, "int4", seed)
+    g = w.WsGemm(M, N, K, tile, stages, 4, 4, dtype, load_path)
+    try:
+        info = g.info.as_dict()
+        if debug:
+            g.set_debug(*debug)
+        C = torch.full((M, N), float("nan"), device="cuda")
+        g(A.cuda(), B.cuda(), C)
+        st = g.sync_status()
+        assert st == w.WS_OK, w.ws_gemm_status_str(st)
+        C = C.cpu().numpy()
+    finally:
+        g.close()
+    rows = sample_rows(M, tile[0], n_random=16, seed=seed)
+    Cref, _ = oracle.gemm_rows(inputs.bits(A), inputs.bits(B), dtype, rows)
+    r = compare_exact(C[rows], Cref)
+    assert r["ok"], r
+    assert exact_checksum(C, A, B, seed), "checksum over all of C differs"
+    return info
+
+
+@pytest.mark.parametrize("load_path", ["registers", "dma"])
+@pytest.mark.parametrize("iters", [1, 2, 3, 7])
+@pytest.mark.parametrize("tile", TILES, ids=lambda t: "x".join(map(str, t)))
+def test_k_iterations_and_ring_depths(tile, iters, load_path):
+    tm, tn, tk = tile
+    M, N, K = 16 * tm, 32 * tn, iters * tk  # 512 tiles: two per workgroup
+    for stages in range(2, min(4, max_stages(tile)) + 1):
+        log("case deep %s S=%d P=%d %s" % (tile, iters, stages, load_path))
+        info = run_and_check(M, N, K, tile, stages, load_path=load_path, seed=100 * iters + stages)
+        assert info["iters"] == iters and info["general"] == 0
+        assert info["tiles"] > info["grid"], "each workgroup must take more than one tile"
+
+
+@pytest.mark.parametrize("tile", TILES, ids=lambda t: "x".join(map(str, t)))
+def test_f16(tile):
+    tm, tn, tk = tile
+    log("case deep f16 %s" % (tile,))
+    run_and_check(8 * tm, 8 * tn, 640, tile, 2, dtype="f16", seed=7)
+
+
+@pytest.mark.parametrize("tile", TILES, ids=lambda t: "x".join(map(str, t)))
+def test_general_variant(tile):
+    # ragged M, N and K: partial tiles zero-filled by the producers
+    tm, tn, tk = tile
+    M, N, K = 5 * tm + 37, 3 * tn + 24, 5 * tk + 40
+    log("case deep general %s %dx%dx%d" % (tile, M, N, K))
+    info = run_and_check(M, N, K, tile, 2, seed=11)
+    assert info["general"] == 1
+
+
+@pytest.mark.parametrize("pdelay,cdelay", [(3, 0), (0, 3), (2, 2)])
+def test_late_producers_and_consumer_delay(pdelay, cdelay):
+    # late producers make the consumer's peek come up short, so it polls
+    log("case deep delays p=%d c=%d" % (pdelay, cdelay))
+    run_and_check(1024, 512, 768, (256, 128, 64), 3, debug=(0, pdelay, cdelay), seed=13)
+
+
+def test_watchdog_reports_timeout_then_recovers():
+    A, B = inputs.make_operands(1024, 512, 1024, "bf16", "int4", 17)
+    log("case deep watchdog")
+    g = w.WsGemm(1024, 512, 1024, (256, 128, 64), 3, 4, 4, "bf16")
+    try:
+        Ad, Bd = A.cuda(), B.cuda()
+        g.set_debug(1, 20, 0)  # one poll allowed, producers ~160k cycles late
+        g(Ad, Bd)
+        assert g.sync_status() == w.WS_ERR_TIMEOUT
+        assert g.sync_status() == w.WS_OK
+        g.set_debug(0, 0, 0)
+        C = g(Ad, Bd)
+        assert g.sync_status() == w.WS_OK
+        Cref, _ = oracle.gemm(inputs.bits(A), inputs.bits(B), "bf16", with_abs=False)
+        assert compare_exact(C.cpu().numpy(), Cref)["ok"]
+    finally:
+        g.close()
