@@ -520,7 +520,8 @@ __device__ __forceinline__ void store_tile(const KernelArgs& args, const f32x16_
         const int dr = mb * 32 + 8 * (e >> 2) + (e & 3);
         char* rowp = cbase + (uint32_t)dr * ldc;
 #pragma unroll
-        for (int nb = 0; nb < BN; ++nb) *(float*)(rowp + lane_off + nb * 128) = acc[mb][nb][e];
+        for (int nb = 0; nb < BN; ++nb)  // non-temporal: C is not read again here, the panels are
+          __builtin_nontemporal_store(acc[mb][nb][e], (float*)(rowp + lane_off + nb * 128));
       }
   }
 }
