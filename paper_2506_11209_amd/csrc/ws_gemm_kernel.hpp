@@ -33,8 +33,9 @@
 //    one producer group and the 128x128, 128x256 and 256x128 tiles, the K
 //    loop of a tile is a generated asm block (consumer_deep,
 //    ws_deep_loop.inc) that keeps the reads of the next k-steps in flight
-//    behind the MFMAs; the other shapes, the event-traced twin and the
-//    register-lean 2:1 variants run compiler-scheduled consumers.
+//    behind the MFMAs; the other shapes, the general variant, the
+//    event-traced twin and the register-lean 2:1 variants run
+//    compiler-scheduled consumers.
 //  * The grid is persistent: at most one workgroup per CU slot, each walking
 //    output tiles in dispatch rounds (Section 2.1, "Wave").  The tile order
 //    places the tiles that run at the same time on one XCD next to each
@@ -1401,10 +1402,11 @@ __global__ void __launch_bounds__((NC + NC * SPLIT) * 64) ws_gemm_kernel(KernelA
       // Three waves per SIMD leave 168 VGPRs: the largest wave tiles then
       // take the single-buffered consumer.
       consumer_rolling<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
-    } else if constexpr (!TRACE && (MODE == kModeGemm || MODE == kModeMath) &&
+    } else if constexpr (!GENERAL && !TRACE && (MODE == kModeGemm || MODE == kModeMath) &&
                          DeepLoop<TM, TN, TK, NC, SPLIT, BF16>::kAvailable) {
       // TK = 64 with one producer group and the three largest tiles: the
-      // hand-scheduled deep-prefetch K loop.
+      // hand-scheduled deep-prefetch K loop (measured slower than the
+      // compiler-scheduled loop in the general variant, so not used there).
       consumer_deep<TM, TN, TK, NC, SPLIT, BF16, MODE, GENERAL>(args, smem, wave, lane);
     } else {
       consumer<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
