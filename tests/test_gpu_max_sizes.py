@@ -3,7 +3,8 @@ kernel's address arithmetic, in the benchmark's launch configuration
 (256x128x64, 3 stages, 4 producer + 4 consumer waves):
 
   * K at the A-panel limit (256 K 2 bytes just below 2^31): 65535
-    K-iterations through one tile;
+    K-iterations through one tile, with a partial tile (general variant) and
+    with one whole tile (plain kernel, deep-prefetch consumer);
   * N at the C-panel limit (256 N 4 bytes just below 2^31);
   * an output of more than 2^32 bytes (M = 2^21, N = 640), with whole tiles
     (plain kernel) and with a partial last tile row (general variant).
@@ -47,6 +48,18 @@ def test_k_at_the_a_panel_limit():
     log("case max K %dx%dx%d" % (M, N, K))
     C, (Cref, S), info = run_rows(M, N, K, "normal", 41, np.arange(M))
     assert info["iters"] == K // 64 and info["general"] == 1
+    r = compare_tol(C, Cref, S, REL_TOL)
+    assert r["ok"], r
+
+
+def test_k_at_the_a_panel_limit_whole_tiles():
+    # one whole 256 x 128 tile: the plain kernel, so the deep-prefetch consumer's
+    # asm K loop runs 65535 K-iterations
+    M, N, K = 256, 128, (1 << 31) // (2 * 256) - 64
+    log("case max K whole tile %dx%dx%d" % (M, N, K))
+    rows = np.array([0, 31, 32, 127, 128, 200, 255])
+    C, (Cref, S), info = run_rows(M, N, K, "normal", 44, rows)
+    assert info["iters"] == K // 64 and info["general"] == 0
     r = compare_tol(C, Cref, S, REL_TOL)
     assert r["ok"], r
 
