@@ -10,12 +10,31 @@ at the loop head (its wait analysis) or, with the reads hidden in asm,
 copies and spills the fragment registers while their reads are still in
 flight.  Here the fragments live in fixed registers at the top of the
 register file (clobbered by the block), the accumulators are operands, and
-every LDS wait is placed by hand.  The schedule and its wait counts are
-explained in ws_gemm_kernel.hpp (consumer_deep).
+every LDS wait is placed by hand.
 
-A K-iteration has four k-steps (TK = 64, one 32x32x16 MFMA per 32x32 block
-and k-step).  Fragment set s (k-step s of a slot) holds BM A fragments
-(ds_read_b128) and BN B fragments (two ds_read_b64_tr_b16 each).
+The schedule, per k-step t of a tile (T = S KS k-steps, KS = TK / 16 per
+K-iteration, one 32x32x16 MFMA per 32x32 block and k-step):
+
+  * wait until the reads of k-step t have landed;
+  * if k-step t + 3 exists: when it starts a new K-iteration, check that
+    K-iteration's slot is full (its counter was peeked when the read stream
+    entered the previous slot; poll, draining every read, only when it is
+    short) and peek at the slot after it; then issue the reads of k-step
+    t + 3, one ahead of each MFMA of k-step t;
+  * when t + 2 ends a K-iteration (t = (u + 1) KS - 2 for K-iteration u),
+    release u's slot: its last reads, for k-step (u + 1) KS - 1, went out at
+    k-step t - 2.
+
+Fragment set s = t mod 4 holds BM A fragments (ds_read_b128) and BN B
+fragments (two ds_read_b64_tr_b16 each).  The loop body is four k-steps
+(4 / KS K-iterations, so a tile needs S KS divisible by 4), preceded by a
+prologue (the reads of k-steps 0-2) and followed by the tile's last four
+k-steps, which read nothing ahead.  A wave's LDS operations complete in
+order, so every wait is "at most n younger LDS operations outstanding"; the
+generator derives each n by replaying the emitted operations along every
+path through the block (prologue, then no loop body up to three, then the
+last four k-steps) and keeping the tightest, capped at 15, the counter's
+range.  The tests replay the emitted text independently.
 """
 from __future__ import annotations
 
@@ -26,16 +45,22 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 OUT = os.path.join(HERE, "ws_deep_loop.inc")
 
 # (TM, TN, TK, NC, SPLIT): the configurations that get the deep consumer
-# (four consumer waves in a 2 x 2 grid, one producer group, TK = 64).
-CONFIGS = [(256, 128, 64, 4, 1), (128, 256, 64, 4, 1), (128, 128, 64, 4, 1)]
+# (four consumer waves in a 2 x 2 grid, one producer group).  Its fixed
+# fragment registers make a kernel take all 256 VGPRs, one workgroup per CU:
+# 128x128x32, whose compiler-scheduled kernel needs 111 and runs two per CU,
+# measured 6 % slower with it and is left out.
+CONFIGS = [(256, 128, 64, 4, 1), (128, 256, 64, 4, 1), (128, 128, 64, 4, 1),
+           (128, 256, 32, 4, 1)]
 HEADER_BYTES = 256
+LGKM_MAX = 15
 
 
 class Cfg:
     def __init__(self, tm, tn, tk, nc, split):
-        assert nc == 4 and split == 1 and tk == 64
+        assert nc == 4 and split == 1 and tk in (32, 64)
         self.tm, self.tn, self.tk, self.nc, self.split = tm, tn, tk, nc, split
         self.np = nc * split
+        self.ks = tk // 16                            # k-steps per K-iteration
         self.wm, self.wn = tm // 2, tn // 2
         self.bm, self.bn = self.wm // 32, self.wn // 32
         self.nq = tn // 16
@@ -44,17 +69,48 @@ class Cfg:
         self.reads = self.bm + 2 * self.bn            # LDS instructions per fragment set
         self.set_regs = 4 * (self.bm + self.bn)
         self.frag_base = 256 - 4 * self.set_regs      # four sets at the top of the file
-        assert self.reads <= 15 and self.bm * self.bn * 16 + 4 * self.set_regs <= 224
-        assert self.stage % 128 == 0 and HEADER_BYTES % 128 == 0
+        assert self.reads <= LGKM_MAX and self.bm * self.bn * 16 + 4 * self.set_regs <= 224
+        assert self.stage % 128 == 0 and HEADER_BYTES % 128 == 0 and 4 % self.ks == 0
 
 
-def gen_block(c: Cfg, bf16: bool) -> list[str]:
-    """Lines of the asm program (operands by name)."""
+class Emitter:
+    """Collects the asm lines of one pass over the block and the tags of its
+    LDS operations in issue order.  A dry run records, for every wait site,
+    how many operations are younger than the last one the site needs; the
+    final pass writes the tightest count over all dry runs."""
+
+    def __init__(self, waits=None):
+        self.lines = []
+        self.ops = []               # tags of LDS operations, oldest first
+        self.waits = waits          # site -> lgkmcnt (final pass) or None (dry run)
+        self.need = {}              # site -> tightest count seen (dry run)
+
+    def emit(self, line):
+        self.lines.append(line)
+
+    def op(self, line, tag):
+        self.lines.append(line)
+        self.ops.append(tag)
+
+    def wait_for(self, site, pred):
+        """s_waitcnt so that every issued operation whose tag satisfies pred
+        has completed."""
+        if self.waits is None:
+            idx = [i for i, t in enumerate(self.ops) if pred(t)]
+            younger = len(self.ops) - 1 - idx[-1] if idx else LGKM_MAX
+            self.need[site] = min(self.need.get(site, LGKM_MAX), younger)
+            self.emit("s_waitcnt lgkmcnt(?)")
+        else:
+            self.emit("s_waitcnt lgkmcnt(%d)" % self.waits[site])
+
+
+def program(E: Emitter, c: Cfg, bf16: bool, S: int | None):
+    """Emit the block.  With S given (a dry run) the loop body is repeated as
+    a tile of S K-iterations runs it, with absolute k-step numbers in the
+    tags; with S None every segment is emitted once."""
     mfma = "v_mfma_f32_32x32x16_bf16" if bf16 else "v_mfma_f32_32x32x16_f16"
-    w2r = min(15, 2 * c.reads)
-    w2r2 = min(15, 2 * c.reads + 2)
-    out = []
-    emit = out.append
+    KS = c.ks
+    emit = E.emit
 
     def a_reg(s, mb):
         b = c.frag_base + s * c.set_regs + 4 * mb
@@ -64,126 +120,72 @@ def gen_block(c: Cfg, bf16: bool) -> list[str]:
         b = c.frag_base + s * c.set_regs + 4 * c.bm + 4 * nb
         return "v[%d:%d]" % (b, b + 3), "v[%d:%d]" % (b, b + 1), "v[%d:%d]" % (b + 2, b + 3)
 
-    def addr(s, base):
-        # the two address registers of fragment set s in the slot at SGPR `base`
-        emit("v_add_u32 %%[va], %%[%s], %%[aoff]" % base)
-        if s:
-            emit("v_xor_b32 %%[va], %d, %%[va]" % (32 * s))
-        emit("v_add_u32 %%[vb], %%[%s], %%[boff]" % base)
+    def addr(kss):
+        # address registers for k-step kss of the slot at SGPR rb: the A chunk
+        # of k-step kss is (2 kss + lane / 32) ^ swz(row), i.e. bits 5.. of the
+        # k-step 0 offset XORed by 32 kss (slots start on 128-byte boundaries)
+        emit("v_add_u32 %[va], %[rb], %[aoff]")
+        if kss:
+            emit("v_xor_b32 %%[va], %d, %%[va]" % (32 * kss))
+        emit("v_add_u32 %[vb], %[rb], %[boff]")
 
-    def reads(s):
+    def reads(t):
+        # (line, tag) of the reads of k-step t into fragment set t mod 4
+        s, kss = t % 4, t % KS
         out = []
         for mb in range(c.bm):
             off = mb * 32 * c.tk * 2
             assert off < 65536
-            out.append("ds_read_b128 %s, %%[va] offset:%d" % (a_reg(s, mb), off))
+            out.append(("ds_read_b128 %s, %%[va] offset:%d" % (a_reg(s, mb), off), ("R", t)))
         for nb in range(c.bn):
             _, lo, hi = b_regs(s, nb)
-            off = ((4 * s) * c.nq + 2 * nb) * 128
+            off = ((4 * kss) * c.nq + 2 * nb) * 128
             assert off + c.nq * 128 < 65536
-            out.append("ds_read_b64_tr_b16 %s, %%[vb] offset:%d" % (lo, off))
-            out.append("ds_read_b64_tr_b16 %s, %%[vb] offset:%d" % (hi, off + c.nq * 128))
+            out.append(("ds_read_b64_tr_b16 %s, %%[vb] offset:%d" % (lo, off), ("R", t)))
+            out.append(("ds_read_b64_tr_b16 %s, %%[vb] offset:%d" % (hi, off + c.nq * 128), ("R", t)))
         return out
 
-    def mfma_list(s):
-        out = []
-        for mb in range(c.bm):
-            for nb in range(c.bn):
-                full, _, _ = b_regs(s, nb)
-                out.append("%s %%[c%d_%d], %s, %s, %%[c%d_%d]" % (mfma, mb, nb, a_reg(s, mb), full, mb, nb))
-        return out
+    def mfma_list(t):
+        s = t % 4
+        return ["%s %%[c%d_%d], %s, %s, %%[c%d_%d]" % (mfma, mb, nb, a_reg(s, mb), b_regs(s, nb)[0], mb, nb)
+                for mb in range(c.bm) for nb in range(c.bn)]
 
-    def issue(s, base):
-        addr(s, base)
-        for l in reads(s):
-            emit(l)
+    def next_slot(slot, target, tmp):
+        # (slot, target) <- those of the next K-iteration: slot + 1 mod P, target + NP on wrap
+        emit("s_add_u32 %%[%s], %%[%s], 1" % (slot, slot))
+        emit("s_add_u32 %%[%s], %%[%s], %d" % (tmp, target, c.np))
+        emit("s_cmp_eq_u32 %%[%s], %%[P]" % slot)
+        emit("s_cselect_b32 %%[%s], 0, %%[%s]" % (slot, slot))
+        emit("s_cselect_b32 %%[%s], %%[%s], %%[%s]" % (target, tmp, target))
 
-    def mfmas(s):
-        for l in mfma_list(s):
-            emit(l)
-
-    def step(s_mfma, s_read, base):
-        # the MFMAs of set s_mfma with the reads of set s_read (in the slot at
-        # `base`) between them: read, MFMA, read, MFMA, ...  A wave tracks at
-        # most 15 LDS operations, so a read can stall at issue; one MFMA after
-        # each keeps the matrix core fed meanwhile (measured faster than
-        # issuing a set's reads together, before or after its MFMAs).
-        addr(s_read, base)
-        ms, rs = mfma_list(s_mfma), reads(s_read)
-        while ms or rs:
-            if rs:
-                emit(rs.pop(0))
-            if ms:
-                emit(ms.pop(0))
-
-    def wait(n):
-        emit("s_waitcnt lgkmcnt(%d)" % n)
-
-    def slot_base(dst, slot):
-        emit("s_mul_i32 %%[%s], %%[%s], %d" % (dst, slot, c.stage))
-        emit("s_add_u32 %%[%s], %%[%s], %%[ring]" % (dst, dst))
-
-    def next_slot():
-        # (ns, nt) <- the slot and full-counter target of the K-iteration after (slot, ft)
-        emit("s_add_u32 %[ns], %[slot], 1")
-        emit("s_add_u32 %%[t0], %%[ft], %d" % c.np)
-        emit("s_cmp_eq_u32 %[ns], %[P]")
-        emit("s_cselect_b32 %[ns], 0, %[ns]")
-        emit("s_cselect_b32 %[nt], %[t0], %[ft]")
-
-    def peek(slot_reg, wrap_next):
-        # issue a read of full[slot] (full[next(slot)] when wrap_next) into vp
-        if wrap_next:
-            emit("s_add_u32 %%[t1], %%[%s], 1" % slot_reg)
-            emit("s_cmp_eq_u32 %[t1], %[P]")
-            emit("s_cselect_b32 %[t1], 0, %[t1]")
-            emit("s_lshl_b32 %[t1], %[t1], 2")
-        else:
-            emit("s_lshl_b32 %%[t1], %%[%s], 2" % slot_reg)
+    def peek(u):
+        # issue a read of full[next(rs)], the counter of K-iteration u, into vp
+        emit("s_add_u32 %[t1], %[rs], 1")
+        emit("s_cmp_eq_u32 %[t1], %[P]")
+        emit("s_cselect_b32 %[t1], 0, %[t1]")
+        emit("s_lshl_b32 %[t1], %[t1], 2")
         emit("s_add_u32 %[t1], %[t1], %[fullb]")
         emit("v_mov_b32 %[vx], %[t1]")
-        emit("ds_read_b32 %[vp], %[vx]")
+        E.op("ds_read_b32 %[vp], %[vx]", ("peek", u))
 
-    def release(n):
-        # one ds_add from lane 0 once at most n younger LDS operations are outstanding
-        emit("s_lshl_b32 %[t1], %[slot], 2")
-        emit("s_add_u32 %[t1], %[t1], %[emptyb]")
-        emit("v_mov_b32 %[vx], %[t1]")
-        emit("v_mov_b32 %[vq], 1")
-        wait(n)
-        emit("s_mov_b64 %[sav], exec")
-        emit("s_mov_b64 exec, 1")
-        emit("ds_add_u32 %[vx], %[vq]")
-        emit("s_mov_b64 exec, %[sav]")
-
-    def delay():
-        emit("s_cmp_le_i32 %[dly], 0")
-        emit("s_cbranch_scc1 6f")
-        emit("s_mov_b32 %[t0], %[dly]")
-        emit("5:")
-        emit("s_sleep 127")
-        emit("s_sub_u32 %[t0], %[t0], 1")
-        emit("s_cmp_lg_u32 %[t0], 0")
-        emit("s_cbranch_scc1 5b")
-        emit("6:")
-
-    def check_next():
-        # vp holds full[ns] as peeked; spin (draining every read) only when short
+    def check(site, u):
+        # K-iteration u (slot rs, target rt) must be full; vp holds its peeked counter
+        E.wait_for(site, lambda tag: tag == ("peek", u))
         emit("v_readfirstlane_b32 %[t0], %[vp]")
-        emit("s_sub_u32 %[t0], %[t0], %[nt]")
+        emit("s_sub_u32 %[t0], %[t0], %[rt]")
         emit("s_cmp_ge_i32 %[t0], 0")
         emit("s_cbranch_scc1 2f")
         emit("s_mov_b32 %[spins], 0")
-        emit("s_lshl_b32 %[t1], %[ns], 2")
+        emit("s_lshl_b32 %[t1], %[rs], 2")
         emit("s_add_u32 %[t1], %[t1], %[fullb]")
         emit("3:")
         emit("v_mov_b32 %[vx], %[t1]")
         emit("ds_read_b32 %[vp], %[vx]")
         emit("v_mov_b32 %[vx], %[abortb]")
         emit("ds_read_b32 %[vq], %[vx]")
-        wait(0)
+        emit("s_waitcnt lgkmcnt(0)")
         emit("v_readfirstlane_b32 %[t0], %[vp]")
-        emit("s_sub_u32 %[t0], %[t0], %[nt]")
+        emit("s_sub_u32 %[t0], %[t0], %[rt]")
         emit("s_cmp_ge_i32 %[t0], 0")
         emit("s_cbranch_scc1 2f")
         emit("v_readfirstlane_b32 %[t0], %[vq]")
@@ -197,85 +199,151 @@ def gen_block(c: Cfg, bf16: bool) -> list[str]:
         emit("s_sleep 1")
         emit("s_branch 3b")
         emit("2:")
-        emit("s_mov_b32 %[st], 0")  # the poll may have set it before a branch not taken
+        emit("s_mov_b32 %[st], 0")  # a poll may have set it before a branch not taken
 
-    # entry: the caller has waited for the first slot of the tile; the
+    def enter(site, u):
+        # the read stream moves on to K-iteration u > 0 of the tile
+        next_slot("rs", "rt", "t0")
+        check(site, u)
+        emit("s_mul_i32 %%[rb], %%[rs], %d" % c.stage)
+        emit("s_add_u32 %[rb], %[rb], %[ring]")
+        peek(u + 1)
+
+    def release(site, u):
+        # K-iteration u's slot (SGPR rel) back to the producers once its reads landed
+        E.wait_for(site, lambda tag: tag[0] == "R" and tag[1] // KS == u)
+        emit("s_lshl_b32 %[t1], %[rel], 2")
+        emit("s_add_u32 %[t1], %[t1], %[emptyb]")
+        emit("v_mov_b32 %[vx], %[t1]")
+        emit("v_mov_b32 %[vq], 1")
+        emit("s_mov_b64 %[sav], exec")
+        emit("s_mov_b64 exec, 1")
+        E.op("ds_add_u32 %[vx], %[vq]", ("rel", u))
+        emit("s_mov_b64 exec, %[sav]")
+        emit("s_add_u32 %[rel], %[rel], 1")
+        emit("s_cmp_eq_u32 %[rel], %[P]")
+        emit("s_cselect_b32 %[rel], 0, %[rel]")
+
+    def delay():
+        emit("s_cmp_le_i32 %[dly], 0")
+        emit("s_cbranch_scc1 6f")
+        emit("s_mov_b32 %[t0], %[dly]")
+        emit("5:")
+        emit("s_sleep 127")
+        emit("s_sub_u32 %[t0], %[t0], 1")
+        emit("s_cmp_lg_u32 %[t0], 0")
+        emit("s_cbranch_scc1 5b")
+        emit("6:")
+
+    def kstep(seg, t, read_ahead):
+        # k-step t; read_ahead: k-step t + 3 exists
+        E.wait_for((seg, t % 4, "R"), lambda tag: tag == ("R", t))
+        ms = mfma_list(t)
+        if read_ahead:
+            if (t + 3) % KS == 0:
+                enter((seg, t % 4, "enter"), (t + 3) // KS)
+            addr((t + 3) % KS)
+            rs = reads(t + 3)
+            # read, MFMA, read, MFMA, ...: a wave tracks at most 15 LDS
+            # operations, so a read can stall at issue; an MFMA after each keeps
+            # the matrix core fed meanwhile (measured faster than issuing a
+            # set's reads together, before or after its MFMAs)
+            while ms or rs:
+                if rs:
+                    E.op(*rs.pop(0))
+                if ms:
+                    emit(ms.pop(0))
+        else:
+            for m in ms:
+                emit(m)
+        if (t + 2) % KS == 0:
+            release((seg, t % 4, "rel"), (t + 2) // KS - 1)
+
+    T = S * KS if S is not None else None
+    # entry: the caller has waited for the tile's first slot (slot, ft); the
     # accumulators were just written by VALU instructions
     emit("s_nop 7")
     emit("s_mov_b32 %[st], 0")
-    slot_base("base", "slot")
-    next_slot()
-    issue(0, "base")
-    issue(1, "base")
-    emit("s_cmp_gt_u32 %[S], 1")
-    emit("s_cbranch_scc0 4f")
-    peek("ns", False)
-    emit("4:")
-    issue(2, "base")
-    emit("s_sub_u32 %[kk], %[S], 1")
+    emit("s_mov_b32 %[rs], %[slot]")
+    emit("s_mov_b32 %[rt], %[ft]")
+    emit("s_mov_b32 %[rel], %[slot]")
+    emit("s_mul_i32 %%[rb], %%[rs], %d" % c.stage)
+    emit("s_add_u32 %[rb], %[rb], %[ring]")
+    peek(1)
+    # prologue: the reads of k-steps 0, 1 and 2
+    for t in range(3):
+        if t and t % KS == 0:
+            enter(("pro", t, "enter"), t // KS)
+        addr(t % KS)
+        for line, tag in reads(t):
+            E.op(line, tag)
+    # S KS / 4 groups of four k-steps: the loop bodies, then the last group
+    emit("s_lshr_b32 %%[kk], %%[S], %d" % {4: 0, 2: 1}[KS])
+    emit("s_sub_u32 %[kk], %[kk], 1")
     emit("s_cmp_eq_u32 %[kk], 0")
     emit("s_cbranch_scc1 8f")
-    # steady K-iteration (the next one is in the same tile)
     emit("1:")
-    delay()
-    wait(w2r)
-    step(0, 3, "base")
-    wait(w2r)
-    check_next()
-    slot_base("nbase", "ns")
-    step(1, 0, "nbase")
-    wait(w2r)
-    step(2, 1, "nbase")
-    release(w2r)
-    peek("ns", True)
-    wait(w2r2)
-    step(3, 2, "nbase")
-    emit("s_mov_b32 %[slot], %[ns]")
-    emit("s_mov_b32 %[ft], %[nt]")
-    emit("s_mov_b32 %[base], %[nbase]")
-    next_slot()
+    for b in range((T // 4 - 1) if S is not None else 1):
+        delay()
+        for j in range(4):
+            kstep("body", 4 * b + j, True)
     emit("s_sub_u32 %[kk], %[kk], 1")
     emit("s_cmp_lg_u32 %[kk], 0")
     emit("s_cbranch_scc1 1b")
-    # last K-iteration of the tile: nothing is read ahead
+    # the tile's last four k-steps: only the first reads ahead
     emit("8:")
     delay()
-    wait(w2r)
-    step(0, 3, "base")
-    wait(w2r)
-    mfmas(1)
-    wait(c.reads)
-    mfmas(2)
-    release(0)
-    mfmas(3)
-    emit("s_mov_b32 %[slot], %[ns]")
-    emit("s_mov_b32 %[ft], %[nt]")
+    t_last = (T - 4) if S is not None else 0
+    for j in range(4):
+        kstep("tail", t_last + j, j == 0)
+    # hand back the slot and target of the next tile's first K-iteration
+    next_slot("rs", "rt", "t0")
+    emit("s_mov_b32 %[slot], %[rs]")
+    emit("s_mov_b32 %[ft], %[rt]")
     emit("9:")
     # the caller reads the accumulators with VALU instructions
     for _ in range(3):
         emit("s_nop 15")
-    return out
+
+
+def tile_iters(c: Cfg):
+    """K-iterations per tile replayed by the dry runs: no loop body, one, two
+    and three (S KS must be a multiple of 4)."""
+    return [n * 4 // c.ks for n in (1, 2, 3, 4)]
+
+
+def gen_block(c: Cfg, bf16: bool) -> list[str]:
+    waits = {}
+    for S in tile_iters(c):
+        E = Emitter()
+        program(E, c, bf16, S)
+        for site, n in E.need.items():
+            waits[site] = min(waits.get(site, LGKM_MAX), n)
+    E = Emitter(waits)
+    program(E, c, bf16, None)
+    return E.lines
 
 
 def gen_struct(c: Cfg, bf16: bool) -> str:
     lines = gen_block(c, bf16)
     acc_ops = ", ".join('[c%d_%d] "+v"(c[%d][%d])' % (mb, nb, mb, nb) for mb in range(c.bm) for nb in range(c.bn))
     clobbers = ", ".join('"v%d"' % r for r in range(c.frag_base, 256))
-    body = "\n".join('        "%s\\n\\t"' % l if not l.endswith(":") else '        "%s\\n\\t"' % l for l in lines)
+    body = "\n".join('        "%s\\n\\t"' % l for l in lines)
     return """template <>
 struct DeepLoop<%(tm)d, %(tn)d, %(tk)d, %(nc)d, %(split)d, %(bf16)s> {
   static constexpr bool kAvailable = true;
+  static constexpr int kIterQuantum = %(quantum)d;  // K-iterations per tile: a multiple of this
   static __device__ __forceinline__ uint32_t tile(f32x16_t (&c)[%(bm)d][%(bn)d], uint32_t a_off0, uint32_t b_off,
                                                   uint32_t& slot, uint32_t& ftarget, uint32_t P, uint32_t S,
                                                   uint32_t ring, uint32_t fullb, uint32_t emptyb, uint32_t abortb,
                                                   int32_t lim, int32_t dly) {
 #if defined(__HIP_DEVICE_COMPILE__)
-    uint32_t st, ns, nt, kk, base, nbase, t0, t1, spins, va, vb, vp, vq, vx;
+    uint32_t st, rs, rt, rb, rel, kk, t0, t1, spins, va, vb, vp, vq, vx;
     uint64_t sav;
     asm volatile(
 %(body)s
-        : %(acc)s, [slot] "+s"(slot), [ft] "+s"(ftarget), [st] "=&s"(st), [ns] "=&s"(ns), [nt] "=&s"(nt),
-          [kk] "=&s"(kk), [base] "=&s"(base), [nbase] "=&s"(nbase), [t0] "=&s"(t0), [t1] "=&s"(t1),
+        : %(acc)s, [slot] "+s"(slot), [ft] "+s"(ftarget), [st] "=&s"(st), [rs] "=&s"(rs), [rt] "=&s"(rt),
+          [rb] "=&s"(rb), [rel] "=&s"(rel), [kk] "=&s"(kk), [t0] "=&s"(t0), [t1] "=&s"(t1),
           [spins] "=&s"(spins), [sav] "=&s"(sav), [va] "=&v"(va), [vb] "=&v"(vb), [vp] "=&v"(vp),
           [vq] "=&v"(vq), [vx] "=&v"(vx)
         : [aoff] "v"(a_off0), [boff] "v"(b_off), [P] "s"(P), [S] "s"(S), [ring] "s"(ring),
@@ -290,7 +358,7 @@ struct DeepLoop<%(tm)d, %(tn)d, %(tk)d, %(nc)d, %(split)d, %(bf16)s> {
   }
 };
 """ % dict(tm=c.tm, tn=c.tn, tk=c.tk, nc=c.nc, split=c.split, bf16="true" if bf16 else "false", bm=c.bm,
-           bn=c.bn, body=body, acc=acc_ops, clobbers=clobbers)
+           bn=c.bn, body=body, acc=acc_ops, clobbers=clobbers, quantum=4 // c.ks)
 
 
 def generate() -> str:
@@ -301,6 +369,7 @@ def generate() -> str:
              "template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16>",
              "struct DeepLoop {",
              "  static constexpr bool kAvailable = false;",
+             "  static constexpr int kIterQuantum = 1;",
              "};",
              ""]
     for t in CONFIGS:

@@ -29,9 +29,10 @@
 //    second half loads B, concurrently (two DMA warps, one tile each).
 //  * Consumers read operands with ds_read_b128 (A, K-contiguous) and
 //    ds_read_b64_tr_b16 (B, N-contiguous, transposed by the read) and
-//    accumulate with v_mfma_f32_32x32x16_{bf16,f16} in fp32.  With TK = 64,
-//    one producer group and the 128x128, 128x256 and 256x128 tiles, the K
-//    loop of a tile is a generated asm block (consumer_deep,
+//    accumulate with v_mfma_f32_32x32x16_{bf16,f16} in fp32.  With one
+//    producer group and the 128x128, 128x256 and 256x128 tiles (TK = 64;
+//    also 128x256 with TK = 32), the K loop of a tile is a generated asm
+//    block (consumer_deep,
 //    ws_deep_loop.inc) that keeps the reads of the next k-steps in flight
 //    behind the MFMAs; the other shapes, the general variant, the
 //    event-traced twin and the register-lean 2:1 variants run
@@ -1092,31 +1093,29 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
 }
 
 // ---------------------------------------------------------------------------
-// Deep-prefetch consumer (four k-steps per K-iteration): the operands of
-// k-step t are read during k-step t - 3, so three k-steps of LDS reads stay in
-// flight behind the MFMAs.  The K loop of a tile is one generated asm block
-// (DeepLoop, ws_deep_loop.inc): its fragment registers are fixed and every
+// Deep-prefetch consumer: the operands of k-step t are read during k-step
+// t - 3, so three k-steps of LDS reads stay in flight behind the MFMAs.  The K
+// loop of a tile is one generated asm block (DeepLoop, ws_deep_loop.inc,
+// written by gen_deep_loop.py): its fragment registers are fixed and every
 // wait on an LDS read is placed by hand.  A wave's LDS operations complete in
 // order, so a wait names how many younger LDS operations may still be
-// outstanding.
+// outstanding; waits cap at 15, the counter's range (a wait for fewer only
+// waits longer).
 //
-// One K-iteration q that is not the last of its tile, in issue order (R_s(q)
-// = the reads of k-step s of q's slot, R = BM + 2 BN instructions):
-//   k-step 0  wait for R_0(q) (2R or more younger);  issue R_3(q);  MFMAs
-//   k-step 1  wait for R_1(q) and the counter peeked at k-step 2 of q - 1
-//             (2R younger); check q + 1's slot is full, polling (and
-//             draining every read) only when it is not; issue R_0(q + 1);
-//             MFMAs
-//   k-step 2  wait for R_2(q) (2R younger);  issue R_1(q + 1);  MFMAs;
-//             release q's slot once R_3(q) has completed (2R younger);
-//             peek at the full counter of q + 2
-//   k-step 3  wait for R_3(q) (2R + 2 younger);  issue R_2(q + 1);  MFMAs
-// Waits cap at 15, the counter's range: a wait for fewer outstanding
-// operations than needed only waits longer.  The last K-iteration of a tile
-// reads nothing ahead and drains (R younger at k-step 2, none at k-step 3);
-// the epilogue follows, and the next tile starts with a prologue: wait for
-// its first slot, issue R_0, R_1, the peek at the following slot (when the
-// tile has a second K-iteration) and R_2.
+// Per k-step t of a tile (KS k-steps per K-iteration, T = S KS in all):
+//   * wait for the reads of k-step t;
+//   * if k-step t + 3 exists and starts a new K-iteration, check that
+//     K-iteration's slot is full (its counter was peeked when the read stream
+//     entered the previous slot; poll, draining every read, only when it is
+//     short) and peek at the next slot's counter; issue the reads of k-step
+//     t + 3, one ahead of each MFMA of k-step t;
+//   * when t + 2 ends a K-iteration, release that K-iteration's slot (its last
+//     reads went out two k-steps earlier).
+// The loop body is four k-steps, so a tile needs S KS divisible by 4
+// (DeepLoop::kIterQuantum); TK = 32 tiles with an odd S take the
+// compiler-scheduled consumer.  The tile's last four k-steps read nothing
+// ahead and drain; the epilogue follows, and the next tile starts with a
+// prologue (the reads of its first three k-steps).
 // ---------------------------------------------------------------------------
 #include "ws_deep_loop.inc"
 
@@ -1125,7 +1124,7 @@ __device__ __forceinline__ void consumer_deep(const KernelArgs& args, WSG_LDS ch
                                               int lane) {
   using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
   using Loop = DeepLoop<TM, TN, TK, NC, SPLIT, BF16>;
-  static_assert(Loop::kAvailable && G::KS == 4, "deep consumer configuration");
+  static_assert(Loop::kAvailable && (G::KS == 4 || G::KS == 2), "deep consumer configuration");
   constexpr int BM = G::BM, BN = G::BN;
   WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
   WSG_LDS uint32_t* empty = full + kMaxStages;
@@ -1144,11 +1143,15 @@ __device__ __forceinline__ void consumer_deep(const KernelArgs& args, WSG_LDS ch
                                     8 * (lane & 15));
   static_assert(kHeaderBytes % 128 == 0 && G::STAGE % 128 == 0, "slots on 128-byte boundaries");
 
+  const uint32_t S = (uint32_t)args.iters;
+  if (S % (uint32_t)Loop::kIterQuantum != 0) {
+    consumer<TM, TN, TK, NC, SPLIT, BF16, false, MODE, GENERAL>(args, smem, cw, lane);
+    return;
+  }
   const int Gd = gridDim.x;
   const int g0 = first_slot(args);
   if (g0 >= args.num_tiles) return;
   const int my_tiles = (args.num_tiles - g0 + Gd - 1) / Gd;
-  const uint32_t S = (uint32_t)args.iters;
   const uint32_t P = (uint32_t)args.stages;
   const uint32_t ring = (uint32_t)(uintptr_t)(smem + kHeaderBytes);
   const uint32_t fullb = (uint32_t)(uintptr_t)full;
@@ -1404,7 +1407,7 @@ __global__ void __launch_bounds__((NC + NC * SPLIT) * 64) ws_gemm_kernel(KernelA
       consumer_rolling<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
     } else if constexpr (!GENERAL && !TRACE && (MODE == kModeGemm || MODE == kModeMath) &&
                          DeepLoop<TM, TN, TK, NC, SPLIT, BF16>::kAvailable) {
-      // TK = 64 with one producer group and the three largest tiles: the
+      // One producer group with the largest tiles (DeepLoop lists them): the
       // hand-scheduled deep-prefetch K loop (measured slower than the
       // compiler-scheduled loop in the general variant, so not used there).
       consumer_deep<TM, TN, TK, NC, SPLIT, BF16, MODE, GENERAL>(args, smem, wave, lane);

@@ -1,10 +1,11 @@
 """The deep-prefetch consumer (generated asm K loop, ws_deep_loop.inc) in every
-configuration that runs it (TK = 64, 4 + 4 waves, 128x128, 128x256 and
-256x128 tiles): its prologue, steady and last K-iterations (1, 2, 3 and 7
-K-iterations per tile), slot wrap-around at every ring depth that fits, two
-output tiles per workgroup, both producer load paths, the polling path (late
-producers), the consumer delay hook and the watchdog.  (The general variant
-of these tiles keeps the compiler-scheduled consumer.)
+configuration that runs it (4 + 4 waves; 128x128, 128x256 and 256x128 tiles
+with TK = 64, 128x256 with TK = 32): its prologue, loop bodies and
+last four k-steps (1-8 K-iterations per tile; TK = 32 tiles with an odd count
+take the compiler-scheduled consumer instead), slot wrap-around at every ring
+depth that fits, two output tiles per workgroup, both producer load paths,
+the polling path (late producers), the consumer delay hook and the watchdog.
+(The general variant of these tiles keeps the compiler-scheduled consumer.)
 
 Operands are small integers, so every product is exact: C is compared with
 the oracle on sampled rows and, over all of C, by an exact checksum
@@ -23,7 +24,7 @@ w = pytest.importorskip("paper_2506_11209_amd.wsgemm")
 pytestmark = pytest.mark.gpu
 
 LDS_LIMIT = 163840
-TILES = [(256, 128, 64), (128, 256, 64), (128, 128, 64)]
+TILES = [(256, 128, 64), (128, 256, 64), (128, 128, 64), (128, 256, 32)]
 
 
 def max_stages(tile):
@@ -62,7 +63,7 @@ def run_and_check(M, N, K, tile, stages, dtype="bf16", load_path="registers", de
 
 
 @pytest.mark.parametrize("load_path", ["registers", "dma"])
-@pytest.mark.parametrize("iters", [1, 2, 3, 7])
+@pytest.mark.parametrize("iters", [1, 2, 3, 4, 7, 8])
 @pytest.mark.parametrize("tile", TILES, ids=lambda t: "x".join(map(str, t)))
 def test_k_iterations_and_ring_depths(tile, iters, load_path):
     tm, tn, tk = tile
