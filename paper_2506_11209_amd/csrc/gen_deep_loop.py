@@ -45,19 +45,25 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 OUT = os.path.join(HERE, "ws_deep_loop.inc")
 
 # (TM, TN, TK, NC, SPLIT): the configurations that get the deep consumer
-# (four consumer waves in a 2 x 2 grid, one producer group).  Its fixed
-# fragment registers make a kernel take all 256 VGPRs, one workgroup per CU:
-# 128x128x32, whose compiler-scheduled kernel needs 111 and runs two per CU,
-# measured 6 % slower with it and is left out.
-CONFIGS = [(256, 128, 64, 4, 1), (128, 256, 64, 4, 1), (128, 128, 64, 4, 1),
-           (128, 256, 32, 4, 1)]
+# (four consumer waves in a 2 x 2 grid).  Its fixed fragment registers make a
+# kernel take all of a wave's registers (256 with one producer group, 168
+# with two).  Left out because they measured slower with it (8192^3):
+# 128x128x32 1:1 (6 %; its compiler-scheduled kernel needs 111 VGPRs and
+# runs two workgroups per CU), 64x128x32 and 128x64x32 1:1 (7-8 %); the
+# 2:1 kernels of the largest tiles run the register-lean consumer.
+CONFIGS = [
+    (256, 128, 64, 4, 1), (128, 256, 64, 4, 1), (128, 128, 64, 4, 1), (64, 128, 64, 4, 1),
+    (128, 64, 64, 4, 1), (128, 256, 32, 4, 1),
+    (128, 128, 64, 4, 2), (128, 64, 64, 4, 2), (64, 128, 64, 4, 2), (64, 64, 64, 4, 2),
+    (128, 128, 32, 4, 2), (128, 64, 32, 4, 2), (64, 128, 32, 4, 2), (64, 64, 32, 4, 2),
+]
 HEADER_BYTES = 256
 LGKM_MAX = 15
 
 
 class Cfg:
     def __init__(self, tm, tn, tk, nc, split):
-        assert nc == 4 and split == 1 and tk in (32, 64)
+        assert nc == 4 and split in (1, 2) and tk in (32, 64)
         self.tm, self.tn, self.tk, self.nc, self.split = tm, tn, tk, nc, split
         self.np = nc * split
         self.ks = tk // 16                            # k-steps per K-iteration
@@ -68,8 +74,10 @@ class Cfg:
         self.stage = self.a_bytes + tk * tn * 2
         self.reads = self.bm + 2 * self.bn            # LDS instructions per fragment set
         self.set_regs = 4 * (self.bm + self.bn)
-        self.frag_base = 256 - 4 * self.set_regs      # four sets at the top of the file
-        assert self.reads <= LGKM_MAX and self.bm * self.bn * 16 + 4 * self.set_regs <= 224
+        # a wave's registers: 256 with two waves per SIMD (4 + 4), 168 with three (4 + 8)
+        self.vgprs = 256 if nc + self.np <= 8 else 168
+        self.frag_base = self.vgprs - 4 * self.set_regs  # four sets at the top of the file
+        assert self.reads <= LGKM_MAX and self.bm * self.bn * 16 + 4 * self.set_regs <= self.vgprs - 32
         assert self.stage % 128 == 0 and HEADER_BYTES % 128 == 0 and 4 % self.ks == 0
 
 
@@ -327,7 +335,7 @@ def gen_block(c: Cfg, bf16: bool) -> list[str]:
 def gen_struct(c: Cfg, bf16: bool) -> str:
     lines = gen_block(c, bf16)
     acc_ops = ", ".join('[c%d_%d] "+v"(c[%d][%d])' % (mb, nb, mb, nb) for mb in range(c.bm) for nb in range(c.bn))
-    clobbers = ", ".join('"v%d"' % r for r in range(c.frag_base, 256))
+    clobbers = ", ".join('"v%d"' % r for r in range(c.frag_base, c.vgprs))
     body = "\n".join('        "%s\\n\\t"' % l for l in lines)
     return """template <>
 struct DeepLoop<%(tm)d, %(tn)d, %(tk)d, %(nc)d, %(split)d, %(bf16)s> {

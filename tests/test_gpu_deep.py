@@ -1,15 +1,18 @@
 """The deep-prefetch consumer (generated asm K loop, ws_deep_loop.inc) in every
-configuration that runs it (4 + 4 waves; 128x128, 128x256 and 256x128 tiles
-with TK = 64, 128x256 with TK = 32): its prologue, loop bodies and
-last four k-steps (1-8 K-iterations per tile; TK = 32 tiles with an odd count
-take the compiler-scheduled consumer instead), slot wrap-around at every ring
-depth that fits, two output tiles per workgroup, both producer load paths,
-the polling path (late producers), the consumer delay hook and the watchdog.
-(The general variant of these tiles keeps the compiler-scheduled consumer.)
+configuration that runs it (the generator's list: one and two producer
+groups, TK = 64 and 32): its prologue, loop bodies and last four k-steps
+(1-8 K-iterations per tile; TK = 32 tiles with an odd count take the
+compiler-scheduled consumer instead), slot wrap-around at every ring depth
+that fits, two output tiles per workgroup, both producer load paths, the
+polling path (late producers), the consumer delay hook and the watchdog.
+(The general variant keeps the compiler-scheduled consumer.)
 
 Operands are small integers, so every product is exact: C is compared with
 the oracle on sampled rows and, over all of C, by an exact checksum
 C x == A (B x) for a random +-1 vector x (fp64, integer-valued sums)."""
+import os
+import sys
+
 import numpy as np
 import pytest
 import torch
@@ -23,8 +26,12 @@ w = pytest.importorskip("paper_2506_11209_amd.wsgemm")
 
 pytestmark = pytest.mark.gpu
 
+sys.path.insert(0, os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                                "paper_2506_11209_amd", "csrc"))
+import gen_deep_loop  # noqa: E402  (the list of deep-consumer configurations)
+
 LDS_LIMIT = 163840
-TILES = [(256, 128, 64), (128, 256, 64), (128, 128, 64), (128, 256, 32)]
+CONFIGS = [(tm, tn, tk, split) for (tm, tn, tk, nc, split) in gen_deep_loop.CONFIGS]
 
 
 def max_stages(tile):
@@ -40,9 +47,9 @@ def exact_checksum(C, A, B, seed):
     return np.array_equal(C.astype(np.float64) @ x, Af @ (Bf @ x))
 
 
-def run_and_check(M, N, K, tile, stages, dtype="bf16", load_path="registers", debug=None, seed=0):
+def run_and_check(M, N, K, tile, stages, dtype="bf16", load_path="registers", debug=None, seed=0, split=1):
     A, B = inputs.make_operands(M, N, K, dtype, "int4", seed)
-    g = w.WsGemm(M, N, K, tile, stages, 4, 4, dtype, load_path)
+    g = w.WsGemm(M, N, K, tile, stages, 4 * split, 4, dtype, load_path)
     try:
         info = g.info.as_dict()
         if debug:
@@ -64,22 +71,23 @@ def run_and_check(M, N, K, tile, stages, dtype="bf16", load_path="registers", de
 
 @pytest.mark.parametrize("load_path", ["registers", "dma"])
 @pytest.mark.parametrize("iters", [1, 2, 3, 4, 7, 8])
-@pytest.mark.parametrize("tile", TILES, ids=lambda t: "x".join(map(str, t)))
-def test_k_iterations_and_ring_depths(tile, iters, load_path):
-    tm, tn, tk = tile
-    M, N, K = 16 * tm, 32 * tn, iters * tk  # 512 tiles: two per workgroup
+@pytest.mark.parametrize("cfg", CONFIGS, ids=lambda t: "%dx%dx%d-%d:1" % t)
+def test_k_iterations_and_ring_depths(cfg, iters, load_path):
+    tm, tn, tk, split = cfg
+    tile = (tm, tn, tk)
+    M, N, K = 16 * tm, 32 * tn, iters * tk  # 512 tiles: two or more per workgroup
     for stages in range(2, min(4, max_stages(tile)) + 1):
-        log("case deep %s S=%d P=%d %s" % (tile, iters, stages, load_path))
-        info = run_and_check(M, N, K, tile, stages, load_path=load_path, seed=100 * iters + stages)
+        log("case deep %s %d:1 S=%d P=%d %s" % (tile, split, iters, stages, load_path))
+        info = run_and_check(M, N, K, tile, stages, load_path=load_path, seed=100 * iters + stages, split=split)
         assert info["iters"] == iters and info["general"] == 0  # the plain kernel: deep consumer
         assert info["tiles"] > info["grid"], "each workgroup must take more than one tile"
 
 
-@pytest.mark.parametrize("tile", TILES, ids=lambda t: "x".join(map(str, t)))
-def test_f16(tile):
-    tm, tn, tk = tile
-    log("case deep f16 %s" % (tile,))
-    run_and_check(8 * tm, 8 * tn, 640, tile, 2, dtype="f16", seed=7)
+@pytest.mark.parametrize("cfg", CONFIGS, ids=lambda t: "%dx%dx%d-%d:1" % t)
+def test_f16(cfg):
+    tm, tn, tk, split = cfg
+    log("case deep f16 %s %d:1" % ((tm, tn, tk), split))
+    run_and_check(8 * tm, 8 * tn, 640, (tm, tn, tk), 2, dtype="f16", seed=7, split=split)
 
 
 @pytest.mark.parametrize("pdelay,cdelay", [(3, 0), (0, 3), (2, 2)])
