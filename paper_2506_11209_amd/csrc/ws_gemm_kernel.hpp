@@ -29,14 +29,13 @@
 //    second half loads B, concurrently (two DMA warps, one tile each).
 //  * Consumers read operands with ds_read_b128 (A, K-contiguous) and
 //    ds_read_b64_tr_b16 (B, N-contiguous, transposed by the read) and
-//    accumulate with v_mfma_f32_32x32x16_{bf16,f16} in fp32.  With one
-//    producer group and the 128x128, 128x256 and 256x128 tiles (TK = 64;
-//    also 128x256 with TK = 32), the K loop of a tile is a generated asm
-//    block (consumer_deep,
-//    ws_deep_loop.inc) that keeps the reads of the next k-steps in flight
-//    behind the MFMAs; the other shapes, the general variant, the
-//    event-traced twin and the register-lean 2:1 variants run
-//    compiler-scheduled consumers.
+//    accumulate with v_mfma_f32_32x32x16_{bf16,f16} in fp32.  In the plain
+//    kernel of most tiles (the list is in gen_deep_loop.py: 1:1 tiles of
+//    64x128 and up, 2:1 tiles up to 128x128) the K loop of a tile is a
+//    generated asm block (consumer_deep, ws_deep_loop.inc) that keeps the
+//    reads of the next k-steps in flight behind the MFMAs; the other shapes,
+//    the general variant, the event-traced twin and the register-lean 2:1
+//    variants of the largest tiles run compiler-scheduled consumers.
 //  * The grid is persistent: at most one workgroup per CU slot, each walking
 //    output tiles in dispatch rounds (Section 2.1, "Wave").  The tile order
 //    places the tiles that run at the same time on one XCD next to each
