@@ -8,7 +8,10 @@ the library (``ws_gemm_create_calibration``) on the launch of an 8192 x 8192
 output (full grid, several rounds; --mn sets another square output):
 
   T_INIT      the empty kernel's time;
-  T_EPILOGUE  (epilogue-only kernel time - T_INIT) / rounds;
+  T_EPILOGUE  (epilogue-only kernel time - T_INIT) / rounds, at least 0
+              (at a one-round launch the difference is a fraction of a
+              microsecond, so both kernels take FIXED_LAUNCHES timed
+              launches);
   T_LOAD-A    load-only time per K-iteration of one workgroup, for two A-tile
               sizes, from the difference of two K so that launch, fill and
               drain cancel;
@@ -51,6 +54,7 @@ TABLE_TILES = {
     "paper": ((64, 64, 64), (64, 128, 64), (128, 64, 64), (128, 128, 64)),
 }
 LDS_LIMIT = 163840
+FIXED_LAUNCHES = 200
 
 
 def stages_for(tile):
@@ -74,6 +78,28 @@ def kernel_us(kind, M, N, K, tile, np_, load_path, A, B, C, steps, warmup):
         return statistics.median(dev) * 1e3, g.info.rounds
     finally:
         g.close()
+
+
+def fixed_costs_us(M, tile, np_, load_path, A, B, C, warmup):
+    """Empty-kernel and epilogue-only-kernel times (us) of one launch point
+    (medians of FIXED_LAUNCHES launches each) and the launch's rounds."""
+    empty = w.WsGemm(M, M, tile[2], tile, stages_for(tile), np_, 4, "bf16", load_path, calibration="empty")
+    epi = w.WsGemm(M, M, tile[2], tile, stages_for(tile), np_, 4, "bf16", load_path, calibration="epilogue")
+    try:
+        st = torch.cuda.current_stream().cuda_stream
+        a, b, c = A.data_ptr(), B.data_ptr(), C.data_ptr()
+        samples = {}
+        for kind, g in (("empty", empty), ("epilogue", epi)):
+            samples[kind], _ = time_launches(lambda: g.run_ptrs(a, b, c, st), FIXED_LAUNCHES, warmup)
+        for g in (empty, epi):
+            s = g.sync_status()
+            if s != w.WS_OK:
+                raise RuntimeError("fixed costs: %s" % w.ws_gemm_status_str(s))
+        return (statistics.median(samples["empty"]) * 1e3, statistics.median(samples["epilogue"]) * 1e3,
+                epi.info.rounds)
+    finally:
+        empty.close()
+        epi.close()
 
 
 def per_iteration_us(kind, tile, np_, load_path, bufs, steps, warmup):
@@ -101,11 +127,10 @@ def calibrate(split, load_path, bufs, steps, warmup, table):
     A, B, C = bufs
     mn = C.shape[0]
     tile0 = PAIRS[split][0]
-    t_init, _ = kernel_us("empty", mn, mn, K_PAIR[0], tile0, np_, load_path, A, B, C, steps, warmup)
-    t_epi_kernel, W = kernel_us("epilogue", mn, mn, tile0[2], tile0, np_, load_path, A, B, C, steps,
-                                warmup)
-    t_epi = (t_epi_kernel - t_init) / W
-    raw = {"t_init_us": t_init, "epilogue_kernel_us": t_epi_kernel, "epilogue_rounds": W}
+    t_init, t_epi_kernel, W = fixed_costs_us(mn, tile0, np_, load_path, A, B, C, warmup)
+    t_epi = max(t_epi_kernel - t_init, 0.0) / W  # a difference within the noise can come out below 0
+    raw = {"t_init_us": t_init, "epilogue_kernel_us": t_epi_kernel, "epilogue_rounds": W,
+           "fixed_cost_launches": FIXED_LAUNCHES}
     loads, loads_b, maths = [], [], []
     for tile in PAIRS[split]:
         tm, tn, tk = tile
