@@ -99,7 +99,7 @@ def main():
     a = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if a.gpus != 1 or world != 1:
-        print("bench.py runs on one GPU only: the GEMM has no multi-GPU path in this build "
+        print("bench.py runs on one GPU only: the GEMM library has no multi-GPU path "
               "(requested --gpus %d, WORLD_SIZE %d)" % (a.gpus, world), file=sys.stderr)
         sys.exit(2)
 
