@@ -4,7 +4,8 @@ kernel's address arithmetic, in the benchmark's launch configuration
 
   * K at the A-panel limit (256 K 2 bytes just below 2^31): 65535
     K-iterations through one tile, with a partial tile (general variant) and
-    with one whole tile (plain kernel, deep-prefetch consumer);
+    with one whole tile (plain kernel, deep-prefetch consumer); also through
+    four 128x64 tiles of the two-producer-group (2:1) deep-prefetch kernel;
   * N at the C-panel limit (256 N 4 bytes just below 2^31);
   * an output of more than 2^32 bytes (M = 2^21, N = 640), with whole tiles
     (plain kernel) and with a partial last tile row (general variant).
@@ -26,9 +27,9 @@ pytestmark = pytest.mark.gpu
 TILE, STAGES, NP, NC = (256, 128, 64), 3, 4, 4
 
 
-def run_rows(M, N, K, dist, seed, rows):
+def run_rows(M, N, K, dist, seed, rows, tile=TILE, stages=STAGES, np_=NP):
     A, B = inputs.make_operands(M, N, K, "bf16", dist, seed)
-    g = w.WsGemm(M, N, K, TILE, STAGES, NP, NC, "bf16")
+    g = w.WsGemm(M, N, K, tile, stages, np_, NC, "bf16")
     try:
         Ad, Bd = A.cuda(), B.cuda()
         C = torch.empty((M, N), dtype=torch.float32, device="cuda")
@@ -60,6 +61,18 @@ def test_k_at_the_a_panel_limit_whole_tiles():
     rows = np.array([0, 31, 32, 127, 128, 200, 255])
     C, (Cref, S), info = run_rows(M, N, K, "normal", 44, rows)
     assert info["iters"] == K // 64 and info["general"] == 0
+    r = compare_tol(C, Cref, S, REL_TOL)
+    assert r["ok"], r
+
+
+def test_k_at_the_a_panel_limit_two_producer_groups():
+    # four whole 128 x 64 tiles of the 2:1 plain kernel (deep-prefetch consumer
+    # with 168 registers a wave), 65535 K-iterations each
+    M, N, K = 256, 128, (1 << 31) // (2 * 256) - 64
+    log("case max K 2:1 128x64x64 %dx%dx%d" % (M, N, K))
+    rows = np.array([0, 63, 127, 128, 191, 255])
+    C, (Cref, S), info = run_rows(M, N, K, "normal", 45, rows, tile=(128, 64, 64), stages=4, np_=8)
+    assert info["iters"] == K // 64 and info["general"] == 0 and info["split"] == 2
     r = compare_tol(C, Cref, S, REL_TOL)
     assert r["ok"], r
 
