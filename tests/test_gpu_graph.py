@@ -21,7 +21,8 @@ pytestmark = pytest.mark.gpu
     ((300, 264, 200), (256, 128, 64), 3, 4, 4, (0.5, 1.0, "bf16")),  # general variant, reads C
     ((256, 256, 0), (128, 128, 32), 3, 4, 4, (1.0, 2.0, "f32")),     # K = 0: the scale kernel
     ((1024, 1024, 448), (256, 128, 64), 3, 4, 4, None),             # deep-prefetch consumer
-], ids=["plain", "general", "k0", "deep"])
+    ((1024, 512, 512), (128, 64, 64), 4, 8, 4, None),               # the same, 2:1
+], ids=["plain", "general", "k0", "deep", "deep-2to1"])
 def test_captured_run_replays_equal_eager(shape, tile, stages, np_, nc, epi):
     M, N, K = shape
     log("case graph %s %s" % (shape, epi))
