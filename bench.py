@@ -6,7 +6,7 @@ M = N = K = 8192, bf16 operands ~ N(0,1), fp32 output.  One step is one full
 C = A B.  Operands are generated once (seeded, synthetic) and are resident in
 HBM before the timed region starts.
 
-    python bench.py [--gpus 1] [--steps 100] [--warmup 50] [--point TMxTNxTKxSxNPxNC]
+    python bench.py [--gpus 1] [--steps 100] [--warmup 50] [--point TMxTNxTKxSxNPxNC[xSPLIT]]
                     [--workload NAME]
 
 Prints one JSON line.  The default workload is the 8192^3 product above;
@@ -32,6 +32,7 @@ DEFAULT_POINT = (256, 128, 64, 3, 4, 4)   # (TM, TN, TK, stages, producer waves,
 DEFAULT_LOAD_PATH = "registers"
 PEAK_TFLOPS = 2500.0                      # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBS = 8000.0                     # MI355X HBM3E
+PEAK_CLOCK_MHZ = 2400.0                   # the clock the MFMA peak is quoted at
 PROFILES = os.path.join(ROOT, "profiles")
 
 
@@ -39,8 +40,9 @@ def kernel_fingerprint(point=DEFAULT_POINT, dtype="bf16") -> str:
     """Hash of the machine code of the GEMM kernel that `point` launches, read
     from the built library (the counter records are tied to that code)."""
     from paper_2506_11209_amd.kernel_code import gemm_symbol, kernel_fingerprint as code_fingerprint
-    tm, tn, tk, _stages, np_, nc = point
-    return code_fingerprint(gemm_symbol(tm, tn, tk, nc, np_ // nc, bf16=(dtype == "bf16")))
+    from paper_2506_11209_amd.workloads import split_of, unpack
+    tm, tn, tk, _stages, np_, nc, _ = unpack(point)
+    return code_fingerprint(gemm_symbol(tm, tn, tk, nc, np_, split_of(point), bf16=(dtype == "bf16")))
 
 
 def traffic_for(point_key: str, point=DEFAULT_POINT, dtype="bf16", workload=WORKLOAD):
@@ -61,30 +63,66 @@ def traffic_for(point_key: str, point=DEFAULT_POINT, dtype="bf16", workload=WORK
     return None
 
 
-def cpu_baseline(wl, target_s: float = 15.0):
-    """The oracle (fp64 triple loop, as committed) on a sample of rows of C."""
+def host_cpu() -> dict:
+    """CPU model and thread counts of this host."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return {"cpu_model": model, "nproc": usable, "logical_cpus": os.cpu_count()}
+
+
+def _oracle_rate(wl, nthreads, target_s, lib):
+    """TFLOP/s of the oracle on the first rows of wl's product (sized to take
+    about target_s), with the number of rows and the seconds."""
     import numpy as np
     import oracle
     from paper_2506_11209_amd import inputs
     A, B = inputs.make_operands(wl.M, wl.N, wl.K, wl.dtype, wl.dist, wl.seed)
     Ab, Bb = inputs.bits(A), inputs.bits(B)
-    lib = oracle.load()
+    threads = nthreads or oracle.max_threads(lib)
     # size the sample from a probe of a few rows per thread (a probe of one
     # row per thread is dominated by thread start-up and undersizes it)
-    cal_rows = min(wl.M, 4 * max(16, oracle.max_threads(lib)))
+    cal_rows = min(wl.M, 4 * max(16 if nthreads != 1 else 2, threads))
     t0 = time.perf_counter()
-    oracle.gemm_rows(Ab, Bb, wl.dtype, np.arange(cal_rows), lib=lib, with_abs=False)
+    oracle.gemm_rows(Ab, Bb, wl.dtype, np.arange(cal_rows), nthreads=nthreads, lib=lib, with_abs=False)
     t_cal = time.perf_counter() - t0
-    rows = int(max(16, min(wl.M, cal_rows * target_s / max(t_cal, 1e-3))))
-    rows -= rows % 16
+    rows = int(max(1, min(wl.M, cal_rows * target_s / max(t_cal, 1e-3))))
+    if rows >= 16:
+        rows -= rows % 16
     t0 = time.perf_counter()
-    oracle.gemm_rows(Ab, Bb, wl.dtype, np.arange(rows), lib=lib, with_abs=False)
+    oracle.gemm_rows(Ab, Bb, wl.dtype, np.arange(rows), nthreads=nthreads, lib=lib, with_abs=False)
     t = time.perf_counter() - t0
-    flops = 2.0 * rows * wl.N * wl.K
-    return {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": oracle.max_threads(lib),
-            "kind": "oracle",
-            "sample": "%d of %d rows of C (%dx%d by %dx%d), including operand decode; %.1f s" % (
-                rows, wl.M, wl.M, wl.K, wl.K, wl.N, t)}
+    return 2.0 * rows * wl.N * wl.K / t / 1e12, rows, t
+
+
+def cpu_baseline(wl, target_s: float = 15.0):
+    """The oracle (fp64 triple loop, as committed) on a sample of rows of C,
+    on all host threads; plus single-thread timings of the 256^3 product
+    (whole) and of a sample of the 4096^3 product."""
+    import oracle
+    from paper_2506_11209_amd.workloads import WORKLOADS
+    lib = oracle.load()
+    value, rows, t = _oracle_rate(wl, 0, target_s, lib)
+    out = {"value": value, "unit": "TFLOP/s", "cores": oracle.max_threads(lib), "kind": "oracle",
+           "sample": "%d of %d rows of C (%dx%d by %dx%d), including operand decode; %.1f s" % (
+               rows, wl.M, wl.M, wl.K, wl.K, wl.N, t)}
+    out.update(host_cpu())
+    single = {}
+    for name, tgt in (("gemm_256x256x256_f16_int4", 1.0), ("gemm_4096x4096x4096_bf16_normal", 6.0)):
+        v, r, ts = _oracle_rate(WORKLOADS[name], 1, tgt, lib)
+        single[name] = {"gflops": round(v * 1e3, 3), "rows": r, "seconds": round(ts, 3)}
+    out["single_thread"] = single
+    return out
 
 
 def main():
@@ -92,10 +130,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--point", default=None, help="TMxTNxTKxSTAGESxNPxNC")
+    ap.add_argument("--point", default=None, help="TMxTNxTKxSTAGESxNPxNC[xSPLIT]")
     ap.add_argument("--load-path", default=DEFAULT_LOAD_PATH, choices=("registers", "dma"))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", default=WORKLOAD)
+    ap.add_argument("--min-warmup-s", type=float, default=0.5,
+                    help="warm up for at least this long, and until two batches of 10 agree within 1%%")
     a = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if a.gpus != 1 or world != 1:
@@ -107,7 +147,7 @@ def main():
     from paper_2506_11209_amd import inputs
     from paper_2506_11209_amd import wsgemm as w
     from paper_2506_11209_amd.timing import summary, time_launches
-    from paper_2506_11209_amd.workloads import WORKLOADS
+    from paper_2506_11209_amd.workloads import WORKLOADS, parse_point, point_key, split_of, unpack
 
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
@@ -117,29 +157,33 @@ def main():
         sys.exit(2)
     wl = WORKLOADS[a.workload]
     if a.point:
-        point = tuple(int(x) for x in a.point.split("x"))
+        point = parse_point(a.point)
     else:
         point = DEFAULT_POINT if wl.name == WORKLOAD else wl.points[0]
-    tm, tn, tk, stages, np_, nc = point
+    tm, tn, tk, stages, np_, nc, split = unpack(point)
     A, B = inputs.make_operands(wl.M, wl.N, wl.K, wl.dtype, wl.dist, wl.seed)
     Ad, Bd = A.cuda(), B.cuda()
     del A, B
     C = torch.empty((wl.M, wl.N), dtype=torch.float32, device="cuda")
-    g = w.WsGemm(wl.M, wl.N, wl.K, (tm, tn, tk), stages, np_, nc, wl.dtype, a.load_path)
+    g = w.WsGemm(wl.M, wl.N, wl.K, (tm, tn, tk), stages, np_, nc, wl.dtype, a.load_path, split=split)
     stream = torch.cuda.current_stream()
     a_p, b_p, c_p, s_p = Ad.data_ptr(), Bd.data_ptr(), C.data_ptr(), stream.cuda_stream
 
     def step():
         g.run_ptrs(a_p, b_p, c_p, s_p)
 
-    dev, wall_ms = time_launches(step, a.steps, a.warmup)
+    # warm up by count and by time (the clock ramps over the first launches);
+    # the launch clock accumulators are cleared just before the timed region
+    dev, wall_ms, wu = time_launches(step, a.steps, a.warmup, min_warmup_s=a.min_warmup_s,
+                                     with_warmup=True, before_timed=lambda: g.clock_mhz(stream))
+    clock_mhz, clock_n = g.clock_mhz(stream)
     st = g.sync_status(stream)
     if st != w.WS_OK:
         print("kernel reported %s" % w.ws_gemm_status_str(st), file=sys.stderr)
         sys.exit(1)
     sm = summary(dev)
     value = wl.flops / (wall_ms * 1e-3) / 1e12
-    pkey = "x".join(map(str, point)) + "/" + a.load_path
+    pkey = point_key(point) + "/" + a.load_path
     # roofline of the kernel: MFMA peak, or HBM bandwidth below the ridge point
     if wl.flops / wl.bytes >= PEAK_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
         bound, unit, peak = "mfma", "TFLOP/s", PEAK_TFLOPS
@@ -167,15 +211,22 @@ def main():
         "pct_mfma_peak": round(100.0 * value / PEAK_TFLOPS, 2),
         "config": {"workload": wl.name, "M": wl.M, "N": wl.N, "K": wl.K,
                    "tile": [tm, tn, tk], "stages": stages, "producer_waves": np_,
-                   "consumer_waves": nc, "split": "%d:1" % (np_ // nc),
+                   "consumer_waves": nc, "split": "%d:1" % split_of(point),
                    "load_path": a.load_path, "grid": g.info.grid, "rounds": g.info.rounds},
         "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak,
                      "unit": unit, "frac": round(achieved / peak, 4),
                      "traffic": traffic_for(pkey, point, wl.dtype, wl.name) if np_ > 0 else None,
-                     "kernel": ("ws_gemm_kernel<%d,%d,%d,%d,%d,%s>" % (tm, tn, tk, nc, np_ // nc, wl.dtype)
+                     "kernel": ("ws_gemm_kernel<%d,%d,%d,%d,%d,%d,%s>" % (tm, tn, tk, nc, np_, split_of(point),
+                                                                          wl.dtype)
                                 if np_ > 0 else "ws_sync_kernel<%d,%d,%d,%d,%s>" % (tm, tn, tk, nc, wl.dtype)),
                      "algorithmic_bytes": wl.bytes, "flop": wl.flops,
-                     "launch_ms": {k: round(v, 5) if isinstance(v, float) else v for k, v in sm.items()}},
+                     "achieved_at_median": round(achieved * sm["mean_ms"] / sm["median_ms"], 2),
+                     "launch_ms": {k: round(v, 5) if isinstance(v, float) else v for k, v in sm.items()},
+                     "clock_mhz": round(clock_mhz, 1) if clock_mhz else None,
+                     "clock_launches": clock_n,
+                     "frac_at_clock": (round(achieved / (peak * clock_mhz / PEAK_CLOCK_MHZ), 4)
+                                       if clock_mhz and bound == "mfma" else None)},
+        "warmup_record": wu,
     }
     g.close()
     if not a.no_cpu_baseline:

@@ -11,11 +11,17 @@
  * wavefronts stream the A and B tiles of every K-iteration into a circular
  * buffer in LDS and consumer (MATH) wavefronts pop them, multiply-accumulate
  * and store the tile (Background, "The Warp Specialized GeMM Kernel in
- * CUTLASS", and Algorithm 1).  Both arrangements of that section exist:
- *   producer_waves == consumer_waves      one DMA warp per MATH warp, loading
- *                                         the A tile and then the B tile;
- *   producer_waves == 2 * consumer_waves  two DMA warps per MATH warp, one
- *                                         loading A and one loading B.
+ * CUTLASS", and Algorithm 1).  The consumer waves of a workgroup act as the
+ * paper's MATH warp and its producer waves as its DMA warp(s).  Both
+ * arrangements of that section exist (`split`):
+ *   split 1  one DMA warp per MATH warp: every producer wave loads its share
+ *            of the A tile and then of the B tile;
+ *   split 2  two DMA warps per MATH warp: half of the producer waves load
+ *            the A tile, the other half the B tile, concurrently.
+ * Wave counts (consumer_waves, producer_waves, split):
+ *   (1, 1, 1), (1, 2, 2), (4, 4, 1), (4, 8, 2), (4, 4, 2),
+ *   (8, 4, 1), (8, 4, 2)  [eight consumer waves: 256 x 256 tiles only],
+ *   and producer_waves = 0: the synchronous (not specialised) kernel.
  * `stages` is the circular buffer's capacity in K-iterations (the buffer of
  * Section 2.2 holding at most a fixed number of tiles).
  *
@@ -58,7 +64,7 @@
 extern "C" {
 #endif
 
-#define WS_GEMM_ABI_VERSION 6
+#define WS_GEMM_ABI_VERSION 7
 
 typedef struct ws_gemm_handle* ws_gemm_t; /* opaque handle */
 
@@ -84,11 +90,13 @@ typedef enum {
 
 typedef struct {
   int32_t tile_m, tile_n, tile_k; /* (T_M, T_N, T_K): powers of two, 32..256 (tile_k 32..128) */
-  int32_t producer_waves;         /* DMA wavefronts per workgroup: consumer_waves or 2x that */
-  int32_t consumer_waves;         /* MATH wavefronts per workgroup: 1 or 4 (one per SIMD) */
+  int32_t producer_waves;         /* DMA wavefronts per workgroup (see the list above) */
+  int32_t consumer_waves;         /* MATH wavefronts per workgroup: 1, 4 (one per SIMD) or 8 (two) */
   int32_t stages;                 /* circular-buffer slots, 2..8 */
   int32_t dtype;                  /* ws_dtype of A and B */
   int32_t load_path;              /* ws_load_path of the producers */
+  int32_t split;                  /* DMA warps per MATH warp, 1 or 2; 0 derives it from the wave
+                                     counts: 2 when producer_waves == 2 consumer_waves, else 1 */
 } ws_gemm_config;
 
 typedef struct {
@@ -166,6 +174,19 @@ ws_status ws_gemm_run(ws_gemm_t h, const void* A, const void* B, void* C, hipStr
 /* Synchronise `stream`, then report and clear the watchdog word:
  * WS_ERR_TIMEOUT if any wait of a previous run on this handle gave up. */
 ws_status ws_gemm_sync_status(ws_gemm_t h, hipStream_t stream);
+
+/* Average shader clock of the runs since the last call (a measurement hook
+ * for reporting a launch's fraction of peak against the clock it ran at).
+ * Every GEMM launch of the handle has workgroup 0's first wave read the
+ * shader-clock counter (s_memtime) and the 100 MHz reference counter
+ * (s_memrealtime) at its start and its end and add the differences to two
+ * device accumulators.  This call synchronises `stream`, returns the sums
+ * and the number of launches they cover, and clears them.  The clock in MHz
+ * is 100 * shader_cycles / ref_ticks.  Every kernel of the handle takes
+ * part (GEMM, its general and traced twins, the calibration kernels) except
+ * the empty calibration kernel and the K = 0 epilogue kernel. */
+ws_status ws_gemm_clock(ws_gemm_t h, hipStream_t stream, uint64_t* shader_cycles,
+                        uint64_t* ref_ticks, int64_t* launches);
 
 /* The plan a handle launches with. */
 ws_status ws_gemm_query(ws_gemm_t h, ws_gemm_plan_info* out);

@@ -51,21 +51,23 @@ OUT = os.path.join(HERE, "ws_deep_loop.inc")
 # 128x128x32 1:1 (6 %; its compiler-scheduled kernel needs 111 VGPRs and
 # runs two workgroups per CU), 64x128x32 and 128x64x32 1:1 (7-8 %); the
 # 2:1 kernels of the largest tiles run the register-lean consumer.
+# (TM, TN, TK, NC, NP): NP producer waves.  Four producer waves serve both
+# the 1:1 arrangement and the 2:1 one with two groups of two (the consumer
+# side is the same); eight are the 2:1 arrangement with two groups of four.
 CONFIGS = [
-    (256, 128, 64, 4, 1), (128, 256, 64, 4, 1), (128, 128, 64, 4, 1), (64, 128, 64, 4, 1),
-    (128, 64, 64, 4, 1), (128, 256, 32, 4, 1),
-    (128, 128, 64, 4, 2), (128, 64, 64, 4, 2), (64, 128, 64, 4, 2), (64, 64, 64, 4, 2),
-    (128, 128, 32, 4, 2), (128, 64, 32, 4, 2), (64, 128, 32, 4, 2), (64, 64, 32, 4, 2),
+    (256, 128, 64, 4, 4), (128, 256, 64, 4, 4), (128, 128, 64, 4, 4), (64, 128, 64, 4, 4),
+    (128, 64, 64, 4, 4), (128, 256, 32, 4, 4),
+    (128, 128, 64, 4, 8), (128, 64, 64, 4, 8), (64, 128, 64, 4, 8), (64, 64, 64, 4, 8),
+    (128, 128, 32, 4, 8), (128, 64, 32, 4, 8), (64, 128, 32, 4, 8), (64, 64, 32, 4, 8),
 ]
 HEADER_BYTES = 256
 LGKM_MAX = 15
 
 
 class Cfg:
-    def __init__(self, tm, tn, tk, nc, split):
-        assert nc == 4 and split in (1, 2) and tk in (32, 64)
-        self.tm, self.tn, self.tk, self.nc, self.split = tm, tn, tk, nc, split
-        self.np = nc * split
+    def __init__(self, tm, tn, tk, nc, np):
+        assert nc == 4 and np in (4, 8) and tk in (32, 64)
+        self.tm, self.tn, self.tk, self.nc, self.np = tm, tn, tk, nc, np
         self.ks = tk // 16                            # k-steps per K-iteration
         self.wm, self.wn = tm // 2, tn // 2
         self.bm, self.bn = self.wm // 32, self.wn // 32
@@ -338,7 +340,7 @@ def gen_struct(c: Cfg, bf16: bool) -> str:
     clobbers = ", ".join('"v%d"' % r for r in range(c.frag_base, c.vgprs))
     body = "\n".join('        "%s\\n\\t"' % l for l in lines)
     return """template <>
-struct DeepLoop<%(tm)d, %(tn)d, %(tk)d, %(nc)d, %(split)d, %(bf16)s> {
+struct DeepLoop<%(tm)d, %(tn)d, %(tk)d, %(nc)d, %(np)d, %(bf16)s> {
   static constexpr bool kAvailable = true;
   static constexpr int kIterQuantum = %(quantum)d;  // K-iterations per tile: a multiple of this
   static __device__ __forceinline__ uint32_t tile(f32x16_t (&c)[%(bm)d][%(bn)d], uint32_t a_off0, uint32_t b_off,
@@ -365,8 +367,287 @@ struct DeepLoop<%(tm)d, %(tn)d, %(tk)d, %(nc)d, %(split)d, %(bf16)s> {
 #endif
   }
 };
-""" % dict(tm=c.tm, tn=c.tn, tk=c.tk, nc=c.nc, split=c.split, bf16="true" if bf16 else "false", bm=c.bm,
+""" % dict(tm=c.tm, tn=c.tn, tk=c.tk, nc=c.nc, np=c.np, bf16="true" if bf16 else "false", bm=c.bm,
            bn=c.bn, body=body, acc=acc_ops, clobbers=clobbers, quantum=4 // c.ks)
+
+
+# ---------------------------------------------------------------------------
+# Register-lean loop for eight consumer waves (two per SIMD) next to four
+# producer waves: twelve waves leave 168 registers a wave, 128 of them the
+# 128 x 64 accumulator, so each fragment is single-buffered and refilled right
+# after its last MFMA of the k-step; the second consumer wave on the SIMD
+# keeps the matrix core busy while one waits for a read.
+#
+# Per k-step t (N-major MFMA order, B fragment nb used by BM consecutive
+# MFMAs, A fragment mb by MFMAs mb and BM + mb):
+#   mfma(0..BM-1, 0); [enter the next slot if t + 1 starts a K-iteration]
+#   read B(t + 1)[0]; mfma(0, 1); [release if t ends a K-iteration]
+#   then mfma(mb, 1), read A(t + 1)[mb] for every mb; read B(t + 1)[1] ...
+# so every read is at least BM - 1 MFMAs of this wave ahead of its use.
+# The A address va and the B address vb move with the read stream: XOR of
+# the k-step bits for A, the slot's byte delta for both.
+# ---------------------------------------------------------------------------
+# (TM, TN, TK, NC, NP)
+ROLL_CONFIGS = [(256, 256, 64, 8, 4), (256, 256, 32, 8, 4)]
+
+
+class RollCfg:
+    def __init__(self, tm, tn, tk, nc, np):
+        assert nc == 8 and np == 4 and tk in (32, 64)
+        self.tm, self.tn, self.tk, self.nc, self.np = tm, tn, tk, nc, np
+        self.ks = tk // 16
+        self.wm, self.wn = tm // 2, tn // 4
+        self.bm, self.bn = self.wm // 32, self.wn // 32
+        self.nq = tn // 16
+        self.a_bytes = tm * tk * 2
+        self.stage = self.a_bytes + tk * tn * 2
+        self.vgprs = 168
+        self.frag_regs = 4 * (self.bm + self.bn)
+        self.frag_base = self.vgprs - self.frag_regs
+        assert self.bn == 2 and self.bm * self.bn * 16 + self.frag_regs <= self.vgprs - 8
+        assert self.stage % 128 == 0 and HEADER_BYTES % 128 == 0
+
+
+# XOR that moves an A address from k-step a to k-step b of a slot
+def _kxor(a, b):
+    return 32 * (a ^ b)
+
+
+def program_roll(E: Emitter, c: RollCfg, bf16: bool, S: int | None):
+    """Emit the roll block (see above).  With S given (a dry run) the loop body
+    is repeated once per K-iteration with absolute k-step numbers in the tags."""
+    mfma = "v_mfma_f32_32x32x16_bf16" if bf16 else "v_mfma_f32_32x32x16_f16"
+    KS = c.ks
+    emit = E.emit
+
+    def a_reg(mb):
+        b = c.frag_base + 4 * mb
+        return "v[%d:%d]" % (b, b + 3)
+
+    def b_reg(nb, part=None):
+        b = c.frag_base + 4 * c.bm + 4 * nb
+        if part is None:
+            return "v[%d:%d]" % (b, b + 3)
+        return "v[%d:%d]" % (b + 2 * part, b + 2 * part + 1)
+
+    def read_a(t, mb):
+        E.op("ds_read_b128 %s, %%[va] offset:%d" % (a_reg(mb), mb * 32 * c.tk * 2), ("A", t, mb))
+
+    def read_b(t, nb):
+        off = ((4 * (t % KS)) * c.nq + 2 * nb) * 128
+        E.op("ds_read_b64_tr_b16 %s, %%[vb] offset:%d" % (b_reg(nb, 0), off), ("B", t, nb))
+        E.op("ds_read_b64_tr_b16 %s, %%[vb] offset:%d" % (b_reg(nb, 1), off + c.nq * 128), ("B", t, nb))
+
+    def mf(mb, nb):
+        emit("%s %%[c%d_%d], %s, %s, %%[c%d_%d]" % (mfma, mb, nb, a_reg(mb), b_reg(nb), mb, nb))
+
+    def next_slot(slot, target, tmp):
+        emit("s_add_u32 %%[%s], %%[%s], 1" % (slot, slot))
+        emit("s_add_u32 %%[%s], %%[%s], %d" % (tmp, target, c.np))
+        emit("s_cmp_eq_u32 %%[%s], %%[P]" % slot)
+        emit("s_cselect_b32 %%[%s], 0, %%[%s]" % (slot, slot))
+        emit("s_cselect_b32 %%[%s], %%[%s], %%[%s]" % (target, tmp, target))
+
+    def peek(u):
+        emit("s_add_u32 %[t1], %[rs], 1")
+        emit("s_cmp_eq_u32 %[t1], %[P]")
+        emit("s_cselect_b32 %[t1], 0, %[t1]")
+        emit("s_lshl_b32 %[t1], %[t1], 2")
+        emit("s_add_u32 %[t1], %[t1], %[fullb]")
+        emit("v_mov_b32 %[vx], %[t1]")
+        E.op("ds_read_b32 %[vp], %[vx]", ("peek", u))
+
+    def check(site, u):
+        E.wait_for(site, lambda tag: tag == ("peek", u))
+        emit("v_readfirstlane_b32 %[t0], %[vp]")
+        emit("s_sub_u32 %[t0], %[t0], %[rt]")
+        emit("s_cmp_ge_i32 %[t0], 0")
+        emit("s_cbranch_scc1 2f")
+        emit("s_mov_b32 %[spins], 0")
+        emit("s_lshl_b32 %[t1], %[rs], 2")
+        emit("s_add_u32 %[t1], %[t1], %[fullb]")
+        emit("3:")
+        emit("v_mov_b32 %[vx], %[t1]")
+        emit("ds_read_b32 %[vp], %[vx]")
+        emit("v_mov_b32 %[vx], %[abortb]")
+        emit("ds_read_b32 %[vq], %[vx]")
+        emit("s_waitcnt lgkmcnt(0)")
+        emit("v_readfirstlane_b32 %[t0], %[vp]")
+        emit("s_sub_u32 %[t0], %[t0], %[rt]")
+        emit("s_cmp_ge_i32 %[t0], 0")
+        emit("s_cbranch_scc1 2f")
+        emit("v_readfirstlane_b32 %[t0], %[vq]")
+        emit("s_cmp_lg_u32 %[t0], 0")
+        emit("s_mov_b32 %[st], 1")
+        emit("s_cbranch_scc1 9f")
+        emit("s_add_u32 %[spins], %[spins], 1")
+        emit("s_cmp_gt_i32 %[spins], %[lim]")
+        emit("s_mov_b32 %[st], 2")
+        emit("s_cbranch_scc1 9f")
+        emit("s_sleep 1")
+        emit("s_branch 3b")
+        emit("2:")
+        emit("s_mov_b32 %[st], 0")
+
+    def enter(site, u):
+        # the read stream moves on to K-iteration u > 0: check its slot is
+        # full, move both addresses by the slot's byte delta, peek at u + 1
+        next_slot("rs", "rt", "t0")
+        check(site, u)
+        emit("s_mov_b32 %[t0], %[rb]")
+        emit("s_mul_i32 %%[rb], %%[rs], %d" % c.stage)
+        emit("s_add_u32 %[rb], %[rb], %[ring]")
+        emit("s_sub_u32 %[t0], %[rb], %[t0]")
+        emit("v_add_u32 %[va], %[t0], %[va]")
+        emit("v_add_u32 %[vb], %[t0], %[vb]")
+        peek(u + 1)
+
+    def release(site, u):
+        E.wait_for(site, lambda tag: tag[0] in ("A", "B") and tag[1] // KS == u)
+        emit("s_lshl_b32 %[t1], %[rel], 2")
+        emit("s_add_u32 %[t1], %[t1], %[emptyb]")
+        emit("v_mov_b32 %[vx], %[t1]")
+        emit("v_mov_b32 %[vq], 1")
+        emit("s_mov_b64 %[sav], exec")
+        emit("s_mov_b64 exec, 1")
+        E.op("ds_add_u32 %[vx], %[vq]", ("rel", u))
+        emit("s_mov_b64 exec, %[sav]")
+        emit("s_add_u32 %[rel], %[rel], 1")
+        emit("s_cmp_eq_u32 %[rel], %[P]")
+        emit("s_cselect_b32 %[rel], 0, %[rel]")
+
+    def delay():
+        emit("s_cmp_le_i32 %[dly], 0")
+        emit("s_cbranch_scc1 6f")
+        emit("s_mov_b32 %[t0], %[dly]")
+        emit("5:")
+        emit("s_sleep 127")
+        emit("s_sub_u32 %[t0], %[t0], 1")
+        emit("s_cmp_lg_u32 %[t0], 0")
+        emit("s_cbranch_scc1 5b")
+        emit("6:")
+
+    def kstep(seg, t, ahead):
+        # k-step t of the tile; ahead: k-step t + 1 exists (read it now)
+        kss = t % KS
+        last_of_iter = kss == KS - 1
+        for mb in range(c.bm):
+            E.wait_for((seg, kss, "a", mb), lambda tag, mb=mb: tag == ("A", t, mb) or
+                       (mb == 0 and tag == ("B", t, 0)))
+            mf(mb, 0)
+        if ahead and last_of_iter:
+            enter((seg, kss, "enter"), (t + 1) // KS)
+        if ahead:
+            read_b(t + 1, 0)
+        E.wait_for((seg, kss, "b1"), lambda tag: tag == ("B", t, 1))
+        mf(0, 1)
+        if last_of_iter:
+            release((seg, kss, "rel"), t // KS)
+        if ahead:
+            emit("v_xor_b32 %%[va], %d, %%[va]" % _kxor(kss, (t + 1) % KS))
+            read_a(t + 1, 0)
+        for mb in range(1, c.bm):
+            mf(mb, 1)
+            if ahead:
+                read_a(t + 1, mb)
+        if ahead:
+            read_b(t + 1, 1)
+
+    # entry: the caller has waited for the tile's first slot (slot, ft) and
+    # pointed va / vb at k-step 0 of it; the accumulators were just written by
+    # VALU instructions
+    emit("s_nop 7")
+    emit("s_mov_b32 %[st], 0")
+    emit("s_mov_b32 %[rs], %[slot]")
+    emit("s_mov_b32 %[rt], %[ft]")
+    emit("s_mov_b32 %[rel], %[slot]")
+    emit("s_mul_i32 %%[rb], %%[rs], %d" % c.stage)
+    emit("s_add_u32 %[rb], %[rb], %[ring]")
+    peek(1)
+    # prologue: the reads of k-step 0, in the order the loop issues them
+    read_b(0, 0)
+    for mb in range(c.bm):
+        read_a(0, mb)
+    read_b(0, 1)
+    # S - 1 loop bodies (one K-iteration each, the last k-step entering the
+    # next slot), then the tile's last K-iteration
+    emit("s_sub_u32 %[kk], %[S], 1")
+    emit("s_cmp_eq_u32 %[kk], 0")
+    emit("s_cbranch_scc1 8f")
+    emit("1:")
+    for u in range((S - 1) if S is not None else 1):
+        delay()
+        for j in range(KS):
+            kstep("body", u * KS + j, True)
+    emit("s_sub_u32 %[kk], %[kk], 1")
+    emit("s_cmp_lg_u32 %[kk], 0")
+    emit("s_cbranch_scc1 1b")
+    emit("8:")
+    delay()
+    u_last = (S - 1) if S is not None else 0
+    for j in range(KS):
+        kstep("tail", u_last * KS + j, j < KS - 1)
+    # hand back the slot and target of the next tile's first K-iteration
+    next_slot("rs", "rt", "t0")
+    emit("s_mov_b32 %[slot], %[rs]")
+    emit("s_mov_b32 %[ft], %[rt]")
+    emit("9:")
+    # nothing of this block may still be in flight (the peek of the next
+    # tile's counter, or reads left by an abort), and the caller reads the
+    # accumulators with VALU instructions
+    emit("s_waitcnt lgkmcnt(0)")
+    for _ in range(3):
+        emit("s_nop 15")
+
+
+def gen_roll_block(c: RollCfg, bf16: bool) -> list[str]:
+    waits = {}
+    for S in (1, 2, 3, 5):
+        E = Emitter()
+        program_roll(E, c, bf16, S)
+        for site, n in E.need.items():
+            waits[site] = min(waits.get(site, LGKM_MAX), n)
+    E = Emitter(waits)
+    program_roll(E, c, bf16, None)
+    return E.lines
+
+
+def gen_roll_struct(c: RollCfg, bf16: bool) -> str:
+    lines = gen_roll_block(c, bf16)
+    acc_ops = ", ".join('[c%d_%d] "+v"(c[%d][%d])' % (mb, nb, mb, nb) for mb in range(c.bm) for nb in range(c.bn))
+    clobbers = ", ".join('"v%d"' % r for r in range(c.frag_base, c.vgprs))
+    body = "\n".join('        "%s\\n\\t"' % l for l in lines)
+    return """template <>
+struct RollLoop<%(tm)d, %(tn)d, %(tk)d, %(nc)d, %(np)d, %(bf16)s> {
+  static constexpr bool kAvailable = true;
+  // va / vb: this lane's A and B read addresses for k-step 0 of the tile's
+  // first slot (moved along by the block).
+  static __device__ __forceinline__ uint32_t tile(f32x16_t (&c)[%(bm)d][%(bn)d], uint32_t va, uint32_t vb,
+                                                  uint32_t& slot, uint32_t& ftarget, uint32_t P, uint32_t S,
+                                                  uint32_t ring, uint32_t fullb, uint32_t emptyb, uint32_t abortb,
+                                                  int32_t lim, int32_t dly) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    uint32_t st, rs, rt, rb, rel, kk, t0, t1, spins, vp, vq, vx;
+    uint64_t sav;
+    asm volatile(
+%(body)s
+        : %(acc)s, [slot] "+s"(slot), [ft] "+s"(ftarget), [st] "=&s"(st), [rs] "=&s"(rs), [rt] "=&s"(rt),
+          [rb] "=&s"(rb), [rel] "=&s"(rel), [kk] "=&s"(kk), [t0] "=&s"(t0), [t1] "=&s"(t1),
+          [spins] "=&s"(spins), [sav] "=&s"(sav), [va] "+v"(va), [vb] "+v"(vb), [vp] "=&v"(vp),
+          [vq] "=&v"(vq), [vx] "=&v"(vx)
+        : [P] "s"(P), [S] "s"(S), [ring] "s"(ring), [fullb] "s"(fullb), [emptyb] "s"(emptyb),
+          [abortb] "s"(abortb), [lim] "s"(lim), [dly] "s"(dly)
+        : "memory", "scc", %(clobbers)s);
+    return st;
+#else
+    (void)c; (void)va; (void)vb; (void)slot; (void)ftarget; (void)P; (void)S; (void)ring;
+    (void)fullb; (void)emptyb; (void)abortb; (void)lim; (void)dly;
+    return 0;
+#endif
+  }
+};
+""" % dict(tm=c.tm, tn=c.tn, tk=c.tk, nc=c.nc, np=c.np, bf16="true" if bf16 else "false", bm=c.bm,
+           bn=c.bn, body=body, acc=acc_ops, clobbers=clobbers)
 
 
 def generate() -> str:
@@ -374,7 +655,7 @@ def generate() -> str:
              "// The K loop of one output tile for the deep-prefetch consumer (consumer_deep",
              "// in ws_gemm_kernel.hpp), one asm block per kernel configuration.",
              "",
-             "template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16>",
+             "template <int TM, int TN, int TK, int NC, int NP, bool BF16>",
              "struct DeepLoop {",
              "  static constexpr bool kAvailable = false;",
              "  static constexpr int kIterQuantum = 1;",
@@ -383,6 +664,15 @@ def generate() -> str:
     for t in CONFIGS:
         for bf16 in (True, False):
             parts.append(gen_struct(Cfg(*t), bf16))
+    parts += ["// The K loop of one output tile for eight consumer waves (consumer_roll).",
+              "template <int TM, int TN, int TK, int NC, int NP, bool BF16>",
+              "struct RollLoop {",
+              "  static constexpr bool kAvailable = false;",
+              "};",
+              ""]
+    for t in ROLL_CONFIGS:
+        for bf16 in (True, False):
+            parts.append(gen_roll_struct(RollCfg(*t), bf16))
     return "\n".join(parts)
 
 

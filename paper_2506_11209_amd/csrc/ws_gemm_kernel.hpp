@@ -98,6 +98,10 @@ struct KernelArgs {
   // General variant only: C <- alpha * (A B) + beta * C, C of type out_dtype.
   float alpha, beta;
   int32_t out_dtype;       // OutType
+  // Launch clock (null: off): workgroup 0's first wave adds the shader-clock
+  // cycles and the 100 MHz reference ticks it spans to clock[0] and clock[1],
+  // and 1 to clock[2]; their ratio is the average shader clock of the launch.
+  unsigned long long* clock;
 };
 
 // Output element type of the general variant's epilogue.
@@ -117,6 +121,34 @@ enum OutType { kOutF32 = 0, kOutBF16 = 1, kOutF16 = 2 };
 constexpr int kTraceEvents = 8;
 // LDS header words holding the producer stamps of each slot (indices 24..55).
 constexpr int kStampIssueA = 24, kStampIssueB = 32, kStampLandA = 40, kStampLandB = 48;
+
+// Launch clock (KernelArgs::clock), taken by one wave at the start and the
+// end of the kernel.  Both counters are read with scalar loads that are
+// waited for at once, so nothing of theirs is in flight afterwards.
+struct LaunchClock {
+  uint64_t c0 = 0, r0 = 0;
+  bool on = false;
+  __device__ __forceinline__ void start(const KernelArgs& args, int wave) {
+    on = args.clock != nullptr && blockIdx.x == 0 && wave == 0;  // wave-uniform
+    if (on) {
+      c0 = __builtin_amdgcn_s_memtime();
+      r0 = __builtin_amdgcn_s_memrealtime();
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    }
+  }
+  __device__ __forceinline__ void stop(const KernelArgs& args, int lane) {
+    if (on) {
+      const uint64_t c1 = __builtin_amdgcn_s_memtime();
+      const uint64_t r1 = __builtin_amdgcn_s_memrealtime();
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      if (lane == 0) {
+        atomicAdd(&args.clock[0], (unsigned long long)(c1 - c0));
+        atomicAdd(&args.clock[1], (unsigned long long)(r1 - r0));
+        atomicAdd(&args.clock[2], 1ull);
+      }
+    }
+  }
+};
 
 // Low 32 bits of the shader-clock counter (s_memtime).
 __device__ __forceinline__ uint32_t cycles32() {
@@ -164,8 +196,10 @@ __device__ __forceinline__ void wait_vmcnt() {
 // mask narrowed to lane 0, so the surrounding code stays branch-free.
 // YOUNGER: how many of this wave's most recent LDS operations may still be
 // outstanding (LDS operations of a wave complete in order, so every older
-// one has completed).  The caller guarantees no scalar-memory load is in
-// flight, since those would share the counter out of order.
+// one has completed).  Scalar-memory loads share the counter and complete
+// out of order, but one in flight only makes the wait stricter: the count
+// bounds LDS and scalar operations together, so when it is at most YOUNGER
+// at most YOUNGER LDS operations are outstanding, and those are the youngest.
 template <int YOUNGER = 0>
 __device__ __forceinline__ void lds_signal(WSG_LDS uint32_t* p) {
   static_assert(YOUNGER >= 0 && YOUNGER <= 15, "lgkmcnt range");
@@ -369,12 +403,12 @@ __device__ __forceinline__ f32x16_t mfma32x32x16(const i16x8_t& a, const i16x8_t
                                                   __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
 }
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16>
+template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16>
 struct Cfg {
-  static constexpr int NP = NC * SPLIT;              // producer waves
+  static constexpr int NP = NPW;                     // producer waves
   static constexpr int NW = NC + NP;                 // waves per workgroup
-  static constexpr int WGM = (NC == 4) ? 2 : 1;      // consumer grid rows
-  static constexpr int WGN = (NC == 4) ? 2 : 1;      // consumer grid cols
+  static constexpr int WGM = (NC >= 4) ? 2 : 1;      // consumer grid rows
+  static constexpr int WGN = (NC == 8) ? 4 : (NC == 4) ? 2 : 1;  // consumer grid cols
   static constexpr int WM = TM / WGM;                // wave tile rows
   static constexpr int WN = TN / WGN;                // wave tile cols
   static constexpr int BM = WM / 32;                 // 32x32 blocks per wave (rows)
@@ -387,8 +421,14 @@ struct Cfg {
   static constexpr int B_INSTR = B_BYTES / 1024;
   static constexpr int CA = TK / 8;                  // 16-byte chunks per A row
   static constexpr int NQ = TN / 16;                 // B blocks per block-row
-  static_assert(NC == 1 || NC == 4, "consumer waves must be 1 or 4");
+  static_assert(NC == 1 || NC == 4 || NC == 8, "consumer waves must be 1, 4 or 8");
   static_assert(SPLIT == 1 || SPLIT == 2, "split must be 1:1 or 2:1");
+  // producer waves: one group of NC (1:1) or two of NC (2:1); with NC = 4 also
+  // two groups of 2 (2:1 at eight waves); with NC = 8 one group of 4 (1:1) or
+  // two of 2 (2:1), twelve waves in all.
+  static_assert((NP == NC * SPLIT && NC != 8) || (NC == 4 && NP == 4) || (NC == 8 && NP == 4),
+                "unsupported producer / consumer arrangement");
+  static_assert(SPLIT == 1 || NP % 2 == 0, "two producer groups need an even number of waves");
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile must be a multiple of 32x32");
   static_assert(TK == 32 || TK == 64 || TK == 128, "TK must be 32, 64 or 128");
   static_assert(A_BYTES % 1024 == 0 && B_BYTES % 1024 == 0, "tiles must be whole KiB");
@@ -559,10 +599,10 @@ __device__ __forceinline__ void wait_landed(uint32_t n) {
   }
 }
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B>
+template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B>
 __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS char* smem,
                                               int a_rank, int b_rank, int lane) {
-  using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
+  using G = Cfg<TM, TN, TK, NC, NPW, SPLIT, BF16>;
   constexpr int A_GROUP = (SPLIT == 1) ? G::NP : G::NP / 2;  // waves sharing the A tile
   constexpr int B_GROUP = (SPLIT == 1) ? G::NP : G::NP / 2;
   constexpr int A_PER = DO_A ? G::A_INSTR / A_GROUP : 0;     // DMA instructions per wave
@@ -682,17 +722,19 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
 // ---------------------------------------------------------------------------
 typedef __attribute__((ext_vector_type(4))) int i32x4_t;
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B,
+template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B,
           bool GENERAL>
 __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LDS char* smem,
                                                   int a_rank, int b_rank, int lane) {
-  using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
+  using G = Cfg<TM, TN, TK, NC, NPW, SPLIT, BF16>;
   constexpr int A_GROUP = (SPLIT == 1) ? G::NP : G::NP / 2;
   constexpr int B_GROUP = (SPLIT == 1) ? G::NP : G::NP / 2;
   constexpr int A_PER = DO_A ? G::A_INSTR / A_GROUP : 0;
   constexpr int B_PER = DO_B ? G::B_INSTR / B_GROUP : 0;
   constexpr int LOADS = A_PER + B_PER;
-  constexpr int STAGE_VGPRS = (G::NW <= 8) ? 152 : 96;
+  // VGPRs for staged tiles: what the consumers' allocation leaves (256 a wave
+  // with eight waves, 168 with twelve)
+  constexpr int STAGE_VGPRS = (G::NW <= 8) ? 152 : (NC == 8 ? 128 : 96);
   constexpr int L0 = STAGE_VGPRS / (4 * LOADS);
   constexpr int L1 = (63 / LOADS) < L0 ? (63 / LOADS) : L0;
   constexpr int L = L1 < 1 ? 1 : (L1 > 6 ? 6 : L1);  // K-iterations staged in VGPRs
@@ -875,38 +917,38 @@ __device__ __forceinline__ void producer_signal_only(const KernelArgs& args, WSG
   }
 }
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B,
+template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B,
           bool GENERAL>
 __device__ __forceinline__ void producer_share(const KernelArgs& args, WSG_LDS char* smem, int a_rank,
                                                int b_rank, int lane) {
   if constexpr (!DO_A && !DO_B) {
     producer_signal_only<NC>(args, smem);
   } else if constexpr (GENERAL) {  // partial tiles possible: always register-staged
-    producer_loop_reg<TM, TN, TK, NC, SPLIT, BF16, TRACE, DO_A, DO_B, true>(args, smem, a_rank, b_rank,
+    producer_loop_reg<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, DO_A, DO_B, true>(args, smem, a_rank, b_rank,
                                                                             lane);
   } else if (args.load_path == 1) {  // wave-uniform: 0 = register-staged, 1 = LDS-DMA
-    producer_loop<TM, TN, TK, NC, SPLIT, BF16, TRACE, DO_A, DO_B>(args, smem, a_rank, b_rank, lane);
+    producer_loop<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, DO_A, DO_B>(args, smem, a_rank, b_rank, lane);
   } else {
-    producer_loop_reg<TM, TN, TK, NC, SPLIT, BF16, TRACE, DO_A, DO_B, false>(args, smem, a_rank, b_rank,
+    producer_loop_reg<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, DO_A, DO_B, false>(args, smem, a_rank, b_rank,
                                                                              lane);
   }
 }
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
+template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
 __device__ __forceinline__ void producer(const KernelArgs& args, WSG_LDS char* smem, int pw,
                                          int lane) {
-  using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
+  using G = Cfg<TM, TN, TK, NC, NPW, SPLIT, BF16>;
   constexpr bool LA = MODE == kModeGemm || MODE == kModeLoadA || MODE == kModeLoadAB;  // A loaded
   constexpr bool LB = MODE == kModeGemm || MODE == kModeLoadB || MODE == kModeLoadAB;  // B loaded
   if constexpr (MODE == kModeEpilogue) {
     return;
   } else if constexpr (SPLIT == 1) {
-    producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, LA, LB, GENERAL>(args, smem, pw, pw, lane);
+    producer_share<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, LA, LB, GENERAL>(args, smem, pw, pw, lane);
   } else {
     if (pw < G::NP / 2)
-      producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, LA, false, GENERAL>(args, smem, pw, 0, lane);
+      producer_share<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, LA, false, GENERAL>(args, smem, pw, 0, lane);
     else
-      producer_share<TM, TN, TK, NC, SPLIT, BF16, TRACE, false, LB, GENERAL>(args, smem, 0,
+      producer_share<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, false, LB, GENERAL>(args, smem, 0,
                                                                            pw - G::NP / 2, lane);
   }
 }
@@ -925,9 +967,9 @@ __device__ __forceinline__ void producer(const KernelArgs& args, WSG_LDS char* s
 // when the producers are ahead.  The slot is released (empty[] signal) right
 // after that k-step's reads are issued, once the older reads have completed.
 // ---------------------------------------------------------------------------
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16>
+template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16>
 struct ConsumerOps {
-  using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
+  using G = Cfg<TM, TN, TK, NC, NPW, SPLIT, BF16>;
   static constexpr int kReads = G::BM + 2 * G::BN;  // LDS reads per k-step
   // A operand of row block mb: 16 bytes per lane at a_src + a_off + mb * 32 rows.
   static __device__ __forceinline__ void load_a(i16x8_t& fa, WSG_LDS char* a_src, uint32_t a_off,
@@ -944,11 +986,11 @@ struct ConsumerOps {
   }
 };
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
+template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
 __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* smem, int cw,
                                          int lane) {
-  using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
-  using Ops = ConsumerOps<TM, TN, TK, NC, SPLIT, BF16>;
+  using G = Cfg<TM, TN, TK, NC, NPW, SPLIT, BF16>;
+  using Ops = ConsumerOps<TM, TN, TK, NC, NPW, SPLIT, BF16>;
   static_assert(G::KS >= 2, "a K-iteration holds at least two k-steps");
   WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
   WSG_LDS uint32_t* empty = full + kMaxStages;
@@ -1118,11 +1160,11 @@ __device__ __forceinline__ void consumer(const KernelArgs& args, WSG_LDS char* s
 // ---------------------------------------------------------------------------
 #include "ws_deep_loop.inc"
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, int MODE, bool GENERAL>
+template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, int MODE, bool GENERAL>
 __device__ __forceinline__ void consumer_deep(const KernelArgs& args, WSG_LDS char* smem, int cw,
                                               int lane) {
-  using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
-  using Loop = DeepLoop<TM, TN, TK, NC, SPLIT, BF16>;
+  using G = Cfg<TM, TN, TK, NC, NPW, SPLIT, BF16>;
+  using Loop = DeepLoop<TM, TN, TK, NC, NPW, BF16>;
   static_assert(Loop::kAvailable && (G::KS == 4 || G::KS == 2), "deep consumer configuration");
   constexpr int BM = G::BM, BN = G::BN;
   WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
@@ -1144,7 +1186,7 @@ __device__ __forceinline__ void consumer_deep(const KernelArgs& args, WSG_LDS ch
 
   const uint32_t S = (uint32_t)args.iters;
   if (S % (uint32_t)Loop::kIterQuantum != 0) {
-    consumer<TM, TN, TK, NC, SPLIT, BF16, false, MODE, GENERAL>(args, smem, cw, lane);
+    consumer<TM, TN, TK, NC, NPW, SPLIT, BF16, false, MODE, GENERAL>(args, smem, cw, lane);
     return;
   }
   const int Gd = gridDim.x;
@@ -1184,6 +1226,72 @@ __device__ __forceinline__ void consumer_deep(const KernelArgs& args, WSG_LDS ch
 }
 
 // ---------------------------------------------------------------------------
+// Consumer of the eight-consumer arrangement (two consumer waves per SIMD,
+// 2 x 4 grid of 128 x 64 wave tiles, next to four producer waves): the K loop
+// of a tile is the generated RollLoop block (ws_deep_loop.inc).  Its
+// fragments are single-buffered and refilled right after their last MFMA of
+// the k-step; the other consumer wave of the SIMD covers the read latency.
+// ---------------------------------------------------------------------------
+template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, int MODE, bool GENERAL>
+__device__ __forceinline__ void consumer_roll(const KernelArgs& args, WSG_LDS char* smem, int cw,
+                                              int lane) {
+  using G = Cfg<TM, TN, TK, NC, NPW, SPLIT, BF16>;
+  using Loop = RollLoop<TM, TN, TK, NC, NPW, BF16>;
+  static_assert(Loop::kAvailable, "roll consumer configuration");
+  constexpr int BM = G::BM, BN = G::BN;
+  WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
+  WSG_LDS uint32_t* empty = full + kMaxStages;
+  WSG_LDS uint32_t* abort_flag = full + 2 * kMaxStages;
+
+  const int wm = cw / G::WGN, wn = cw % G::WGN;
+  // A operand of k-step 0: row r, 16-byte chunk (lane / 32) ^ swz(r); the
+  // block moves it to k-step s by XORing 32 s into the byte offset.
+  const int r = wm * G::WM + (lane & 31);
+  const uint32_t a_off0 = (uint32_t)(r * TK * 2 + (((lane >> 5) ^ swz_a<TK>(r)) << 4));
+  const int grp = lane >> 4;
+  const uint32_t b_off = (uint32_t)(G::A_BYTES +
+                                    ((2 * (grp >> 1)) * G::NQ + (wn * G::WN) / 16 + (grp & 1)) * 128 +
+                                    8 * (lane & 15));
+  static_assert(kHeaderBytes % 128 == 0 && G::STAGE % 128 == 0, "slots on 128-byte boundaries");
+
+  const int Gd = gridDim.x;
+  const int g0 = first_slot(args);
+  if (g0 >= args.num_tiles) return;
+  const int my_tiles = (args.num_tiles - g0 + Gd - 1) / Gd;
+  const uint32_t P = (uint32_t)args.stages;
+  const uint32_t S = (uint32_t)args.iters;
+  const uint32_t ring = (uint32_t)(uintptr_t)(smem + kHeaderBytes);
+  const uint32_t fullb = (uint32_t)(uintptr_t)full;
+  const uint32_t emptyb = (uint32_t)(uintptr_t)empty;
+  const uint32_t abortb = (uint32_t)(uintptr_t)abort_flag;
+
+  int v = g0, ti, tj;
+  tile_coords(v, args.tiles_m, args.tiles_n, args.group_m, &ti, &tj);
+  f32x16_t acc[BM][BN];
+  uint32_t slot = 0, ftarget = (uint32_t)G::NP;  // K-iteration 0: ring_slot 0, ring_full_target NP
+  for (int t = 0; t < my_tiles; ++t) {
+#pragma unroll
+    for (int mb = 0; mb < BM; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < BN; ++nb) acc[mb][nb] = f32x16_t{};
+    if (!wait_counter(&full[slot], ftarget, abort_flag, args.spin_limit, args.err)) return;
+    const uint32_t base = ring + slot * (uint32_t)G::STAGE;
+    const uint32_t st = Loop::tile(acc, base + a_off0, base + b_off, slot, ftarget, P, S, ring, fullb,
+                                   emptyb, abortb, args.spin_limit, args.consumer_delay);
+    if (st != 0) {
+      if (st == 2) report_timeout(abort_flag, args.err);
+      return;
+    }
+    // The calibration MATH kernel keeps its products (the store below is
+    // never taken: M > 0) without writing C.
+    if (MODE != kModeMath || args.M < 0)
+      store_tile<TM, TN, G::WM, G::WN, BM, BN, GENERAL, 1>(args, acc, ti, tj, wm, wn, lane);
+    v += Gd;
+    tile_coords(v, args.tiles_m, args.tiles_n, args.group_m, &ti, &tj);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Register-lean consumer for three waves per SIMD (two producers per consumer
 // with the largest wave tiles): every operand fragment is single-buffered and
 // refilled right after its last MFMA of the k-step, and the loop body is one
@@ -1191,11 +1299,11 @@ __device__ __forceinline__ void consumer_deep(const KernelArgs& args, WSG_LDS ch
 // Waits and releases are branch-free asm blocks enabled on the last k-step
 // of a K-iteration.  Same synchronisation as consumer().
 // ---------------------------------------------------------------------------
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
+template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
 __device__ __forceinline__ void consumer_rolling(const KernelArgs& args, WSG_LDS char* smem, int cw,
                                                  int lane) {
-  using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
-  using Ops = ConsumerOps<TM, TN, TK, NC, SPLIT, BF16>;
+  using G = Cfg<TM, TN, TK, NC, NPW, SPLIT, BF16>;
+  using Ops = ConsumerOps<TM, TN, TK, NC, NPW, SPLIT, BF16>;
   WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
   WSG_LDS uint32_t* empty = full + kMaxStages;
   WSG_LDS uint32_t* abort_flag = full + 2 * kMaxStages;
@@ -1354,9 +1462,9 @@ __device__ __forceinline__ void consumer_release_only(const KernelArgs& args, WS
   }
 }
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16>
+template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16>
 __device__ __forceinline__ void consumer_epilogue_only(const KernelArgs& args, int cw, int lane) {
-  using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
+  using G = Cfg<TM, TN, TK, NC, NPW, SPLIT, BF16>;
   const int wm = cw / G::WGN, wn = cw % G::WGN;
   f32x16_t acc[G::BM][G::BN];
 #pragma unroll
@@ -1386,36 +1494,43 @@ __global__ void __launch_bounds__(256) ws_scale_kernel(void* C, int64_t n, float
 template <int UNUSED = 0>
 __global__ void __launch_bounds__(1024) ws_empty_kernel(KernelArgs) {}
 
-template <int TM, int TN, int TK, int NC, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
-__global__ void __launch_bounds__((NC + NC * SPLIT) * 64) ws_gemm_kernel(KernelArgs args) {
-  using G = Cfg<TM, TN, TK, NC, SPLIT, BF16>;
+template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
+__global__ void __launch_bounds__((NC + NPW) * 64) ws_gemm_kernel(KernelArgs args) {
+  using G = Cfg<TM, TN, TK, NC, NPW, SPLIT, BF16>;
   extern __shared__ __attribute__((aligned(1024))) char smem_generic[];
   WSG_LDS char* smem = (WSG_LDS char*)smem_generic;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
+  LaunchClock clk;
+  clk.start(args, wave);
   if (threadIdx.x < 2 * kMaxStages + 1) ((WSG_LDS uint32_t*)smem)[threadIdx.x] = 0u;
   __syncthreads();
   if (wave < NC) {
     if constexpr (MODE == kModeLoadA || MODE == kModeLoadB || MODE == kModeLoadAB) {
       consumer_release_only<G::NP, NC>(args, smem);
     } else if constexpr (MODE == kModeEpilogue) {
-      consumer_epilogue_only<TM, TN, TK, NC, SPLIT, BF16>(args, wave, lane);
+      consumer_epilogue_only<TM, TN, TK, NC, NPW, SPLIT, BF16>(args, wave, lane);
+    } else if constexpr (!GENERAL && !TRACE && (MODE == kModeGemm || MODE == kModeMath) &&
+                         RollLoop<TM, TN, TK, NC, NPW, BF16>::kAvailable) {
+      // Eight consumer waves: the generated register-lean K loop.
+      consumer_roll<TM, TN, TK, NC, NPW, SPLIT, BF16, MODE, GENERAL>(args, smem, wave, lane);
     } else if constexpr (G::NW > 8 && G::BM * G::BN >= 8) {
       // Three waves per SIMD leave 168 VGPRs: the largest wave tiles then
       // take the single-buffered consumer.
-      consumer_rolling<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
+      consumer_rolling<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
     } else if constexpr (!GENERAL && !TRACE && (MODE == kModeGemm || MODE == kModeMath) &&
-                         DeepLoop<TM, TN, TK, NC, SPLIT, BF16>::kAvailable) {
+                         DeepLoop<TM, TN, TK, NC, NPW, BF16>::kAvailable) {
       // One producer group with the largest tiles (DeepLoop lists them): the
       // hand-scheduled deep-prefetch K loop (measured slower than the
       // compiler-scheduled loop in the general variant, so not used there).
-      consumer_deep<TM, TN, TK, NC, SPLIT, BF16, MODE, GENERAL>(args, smem, wave, lane);
+      consumer_deep<TM, TN, TK, NC, NPW, SPLIT, BF16, MODE, GENERAL>(args, smem, wave, lane);
     } else {
-      consumer<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
+      consumer<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
     }
   } else {
-    producer<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave - NC, lane);
+    producer<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave - NC, lane);
   }
+  clk.stop(args, lane);
 }
 
 }  // namespace wsg

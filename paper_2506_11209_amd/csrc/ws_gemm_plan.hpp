@@ -43,6 +43,7 @@ struct PlanIn {
   int64_t M, N, K;
   int32_t tile_m, tile_n, tile_k;
   int32_t producer_waves, consumer_waves, stages, dtype, load_path;
+  int32_t split;       // DMA warps per MATH warp (1 or 2); 0: derived from the wave counts
   int32_t num_cus;     // compute units on the device
   int32_t wgs_per_cu;  // resident workgroups per CU (<= 0: derive from LDS, waves and registers)
   int32_t vgprs, agprs;  // registers per wave of the kernel (0: unknown, not a limit)
@@ -82,6 +83,18 @@ inline int waves_per_simd_by_regs(int vgprs, int agprs) {
   return w < kMaxWavesPerSimd ? w : kMaxWavesPerSimd;
 }
 
+// DMA warps per MATH warp of a wave arrangement (consumer waves nc, producer
+// waves np, requested split; 0 requests the one the wave counts imply), or
+// -1 when no kernel has that arrangement.  0 for the synchronous kernel.
+inline int arrangement_split(int nc, int np, int split) {
+  if (np == 0) return (nc == 1 || nc == 4) && split == 0 ? 0 : -1;
+  if (split == 0) split = (np == 2 * nc) ? 2 : 1;
+  if (nc == 1) return (np == split) ? split : -1;
+  if (nc == 4) return (np == 4 || (np == 8 && split == 2)) ? split : -1;
+  if (nc == 8) return np == 4 ? split : -1;
+  return -1;
+}
+
 inline bool is_pow2_in(int x, int lo, int hi) {
   return x >= lo && x <= hi && (x & (x - 1)) == 0;
 }
@@ -98,11 +111,13 @@ inline int plan_launch(const PlanIn& in, PlanOut* out) {
       !is_pow2_in(in.tile_k, 32, 128))
     return kPlanInvalid;
   const int nc = in.consumer_waves, np = in.producer_waves;
-  if (nc != 1 && nc != 4) return kPlanUnsupported;
+  if (in.split < 0 || in.split > 2) return kPlanInvalid;
+  if (nc != 1 && nc != 4 && nc != 8) return kPlanUnsupported;
   // np == 0: the synchronous kernel (every wave loads and computes), ring
   // depth 1 (no overlap) or 2 (double-buffered).
-  if (np != 0 && np != nc && np != 2 * nc) return kPlanUnsupported;
-  const int wm = in.tile_m / (nc == 4 ? 2 : 1), wn = in.tile_n / (nc == 4 ? 2 : 1);
+  const int split = arrangement_split(nc, np, in.split);
+  if (split < 0) return kPlanUnsupported;
+  const int wm = in.tile_m / (nc >= 4 ? 2 : 1), wn = in.tile_n / (nc == 8 ? 4 : nc == 4 ? 2 : 1);
   // Wave tiles hold their fp32 accumulators in registers: up to 128 x 64 when
   // producer waves share the SIMDs, up to 128 x 128 when they do not.
   if (wm < 32 || wn < 32 || wm * wn > (np == 0 ? 128 * 128 : 128 * 64)) return kPlanUnsupported;
@@ -121,7 +136,7 @@ inline int plan_launch(const PlanIn& in, PlanOut* out) {
     out->tiles_m = (int32_t)((in.M + in.tile_m - 1) / in.tile_m);
     out->tiles_n = (int32_t)((in.N + in.tile_n - 1) / in.tile_n);
     out->iters = (int32_t)((in.K + in.tile_k - 1) / in.tile_k);
-    out->split = np / nc;
+    out->split = split;
     out->group_m = 1;
     return kPlanOk;
   }
@@ -178,7 +193,7 @@ inline int plan_launch(const PlanIn& in, PlanOut* out) {
   out->tiles = tiles;
   out->rounds = (tiles + grid - 1) / grid;
   out->iters = (int32_t)((in.K + in.tile_k - 1) / in.tile_k);
-  out->split = np / nc;  // 0 for the synchronous kernel
+  out->split = split;  // 0 for the synchronous kernel
   out->group_m = best_gm;
   out->xcd_remap = xcd_remap;
   out->ragged = ragged ? 1 : 0;

@@ -42,6 +42,8 @@ __global__ void __launch_bounds__(NC * 64) ws_sync_kernel(KernelArgs args) {
   const int lane = threadIdx.x & 63;
   const int K = args.K, N = args.N;
   const int P = args.stages;  // 1: synchronous; 2: double-buffered
+  LaunchClock clk;
+  clk.start(args, wave);
 
   // This wave's share of every tile, as in the producers of the specialised
   // kernel: chunk (wave + n * NC) * 64 + lane of the LDS tile.
@@ -155,6 +157,7 @@ __global__ void __launch_bounds__(NC * 64) ws_sync_kernel(KernelArgs args) {
     store_tile<TM, TN, G::WM, G::WN, G::BM, G::BN>(args, acc, ti, tj, wm, wn, lane);
   }
   wait_vmcnt<0>();  // no load into LDS outlives the workgroup
+  clk.stop(args, lane);
 }
 
 }  // namespace wsg

@@ -97,7 +97,8 @@ def kernel_fingerprint(symbol: str, lib_path: str | None = None) -> str:
     raise LookupError("kernel %s not found in %s" % (symbol, lib_path))
 
 
-def gemm_symbol(tm, tn, tk, consumer_waves, split, bf16=True, trace=False, mode=0, general=False) -> str:
-    """Mangled name of ws_gemm_kernel<TM, TN, TK, NC, SPLIT, BF16, TRACE, MODE, GENERAL>."""
-    return ("_ZN3wsg14ws_gemm_kernelILi%dELi%dELi%dELi%dELi%dELb%dELb%dELi%dELb%dEEEvNS_10KernelArgsE"
-            % (tm, tn, tk, consumer_waves, split, int(bf16), int(trace), mode, int(general)))
+def gemm_symbol(tm, tn, tk, consumer_waves, producer_waves, split, bf16=True, trace=False, mode=0,
+                general=False) -> str:
+    """Mangled name of ws_gemm_kernel<TM, TN, TK, NC, NP, SPLIT, BF16, TRACE, MODE, GENERAL>."""
+    return ("_ZN3wsg14ws_gemm_kernelILi%dELi%dELi%dELi%dELi%dELi%dELb%dELb%dELi%dELb%dEEEvNS_10KernelArgsE"
+            % (tm, tn, tk, consumer_waves, producer_waves, split, int(bf16), int(trace), mode, int(general)))

@@ -103,10 +103,11 @@ def compiled_configs(dtype="bf16", splits=(1, 2), consumer_waves=(4,)):
     from paper_2506_11209_amd.build import MODE_GEMM, instances
     want_bf16 = 1 if dtype == "bf16" else 0
     out = set()
-    for (tm, tn, tk, nc, split, bf16, trace, mode, general) in instances():
+    for (tm, tn, tk, nc, np_, split, bf16, trace, mode, general) in instances():
+        # the arrangements the calibration covers: split groups of nc producer waves
         if (bf16 == want_bf16 and not trace and not general and mode == MODE_GEMM and split in splits
-                and nc in consumer_waves):
-            out.add(((tm, tn, tk), nc * split, nc))
+                and nc in consumer_waves and np_ == nc * split):
+            out.add(((tm, tn, tk), np_, nc))
     return sorted(out)
 
 

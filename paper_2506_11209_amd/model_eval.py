@@ -37,7 +37,7 @@ import torch
 from paper_2506_11209_amd import wsgemm as w
 from paper_2506_11209_amd.model import load_calibration, load_cost_table, predict, predict_costs
 from paper_2506_11209_amd.timing import time_launches
-from paper_2506_11209_amd.workloads import WORKLOADS
+from paper_2506_11209_amd.workloads import WORKLOADS, split_of, unpack
 
 LDS_LIMIT = 163840
 
@@ -64,9 +64,12 @@ def accuracy_grid():
 def bench_grid():
     wl = WORKLOADS["gemm_8192x8192x8192_bf16_normal"]
     out = []
-    for (tm, tn, tk, P, np_, nc) in wl.points:
-        if np_ > 0 and fits((tm, tn, tk), P):  # the synchronous kernel's points have no producers
-            out.append((wl.M, wl.N, wl.K, (tm, tn, tk), P, np_ // nc))
+    for pt in wl.points:
+        tm, tn, tk, P, np_, nc, _ = unpack(pt)
+        # the synchronous kernel's points have no producers; the model is
+        # calibrated for split groups of four producer waves
+        if np_ > 0 and np_ == nc * split_of(pt) and nc == 4 and fits((tm, tn, tk), P):
+            out.append((wl.M, wl.N, wl.K, (tm, tn, tk), P, split_of(pt)))
     return out
 
 

@@ -72,7 +72,8 @@ def traffic(fetch_db, write_db, cal_fetch_db, cal_write_db, kernel, point, copy_
     import sys
     sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
     from bench import WORKLOAD, kernel_fingerprint
-    point_t = tuple(int(x) for x in point.split("/")[0].split("x"))
+    from paper_2506_11209_amd.workloads import parse_point
+    point_t = parse_point(point.split("/")[0])
     copy_bytes = copy_mib * (1 << 20)
     f_scale = copy_bytes / (_mean_counter(cal_fetch_db, "copyBuffer", "FETCH_SIZE") * 1024)
     w_scale = copy_bytes / (_mean_counter(cal_write_db, "copyBuffer", "WRITE_SIZE") * 1024)

@@ -25,22 +25,18 @@ import torch
 from paper_2506_11209_amd import inputs
 from paper_2506_11209_amd import wsgemm as w
 from paper_2506_11209_amd.timing import summary, time_launches
-from paper_2506_11209_amd.workloads import WORKLOADS
+from paper_2506_11209_amd.workloads import WORKLOADS, parse_point, point_key, split_of, unpack
 
 PEAK_TFLOPS = {"bf16": 2500.0, "f16": 2500.0}  # MI355X dense MFMA
 PEAK_HBM_GBS = 8000.0
 
 
-def point_key(p):
-    return "x".join(str(x) for x in p)
-
-
-def measure_point(wl, point, Ad, Bd, C, steps, warmup, load_path="registers"):
-    tm, tn, tk, stages, np_, nc = point
-    cfg = w.config((tm, tn, tk), stages, np_, nc, wl.dtype, load_path)
+def measure_point(wl, point, Ad, Bd, C, steps, warmup, load_path="registers", min_warmup_s=0.3):
+    tm, tn, tk, stages, np_, nc, split = unpack(point)
+    cfg = w.config((tm, tn, tk), stages, np_, nc, wl.dtype, load_path, split)
     s, h = w.ws_gemm_create(wl.M, wl.N, wl.K, cfg)
     rec = {"workload": wl.name, "tile": [tm, tn, tk], "stages": stages, "producer_waves": np_,
-           "consumer_waves": nc, "split": "%d:1" % (np_ // nc), "load_path": load_path,
+           "consumer_waves": nc, "split": "%d:1" % split_of(point), "load_path": load_path,
            "point": point_key(point) + "/" + load_path}
     if s != w.WS_OK:
         rec["status"] = w.ws_gemm_status_str(s)
@@ -55,7 +51,10 @@ def measure_point(wl, point, Ad, Bd, C, steps, warmup, load_path="registers"):
             if st != w.WS_OK:
                 raise RuntimeError(w.ws_gemm_status_str(st))
 
-        dev, wall = time_launches(launch, steps, warmup)
+        dev, wall = time_launches(launch, steps, warmup, min_warmup_s=min_warmup_s,
+                                  before_timed=lambda: w.ws_gemm_clock(h, stream))
+        _, cyc, ticks, nclk = w.ws_gemm_clock(h, stream)
+        rec["clock_mhz"] = 100.0 * cyc / ticks if ticks else None
         st = w.ws_gemm_sync_status(h, stream)
         if st != w.WS_OK:
             rec["status"] = w.ws_gemm_status_str(st)
@@ -73,6 +72,8 @@ def measure_point(wl, point, Ad, Bd, C, steps, warmup, load_path="registers"):
     rec.update({
         "status": "ok", "plan": info.as_dict(), "device_ms": sm, "wall_ms_per_launch": wall,
         "tflops": tflops, "frac_mfma_peak": tflops / PEAK_TFLOPS[wl.dtype],
+        "frac_mfma_peak_at_clock": (tflops / (PEAK_TFLOPS[wl.dtype] * rec["clock_mhz"] / 2400.0)
+                                    if rec.get("clock_mhz") else None),
         "hbm_gbs_algorithmic": wl.bytes / t / 1e9, "frac_hbm_roofline": wl.bytes / t / 1e9 / PEAK_HBM_GBS,
         "max_scaled_err": max_scaled_err,
     })
@@ -93,7 +94,7 @@ def main(argv=None):
     wl = WORKLOADS[a.workload]
     points = wl.points
     if a.points:
-        points = tuple(tuple(int(x) for x in p.split("x")) for p in a.points.split(","))
+        points = tuple(parse_point(p) for p in a.points.split(","))
     done = set()
     if a.out and os.path.exists(a.out):
         for line in open(a.out):

@@ -1,7 +1,7 @@
 """Event traces of the warp-specialised GEMM (the events of the paper's
 Section 2.2, measured on the GPU).
 
-    python -m paper_2506_11209_amd.trace [--workload NAME] [--point TMxTNxTKxSxNPxNC] [--wgs 4]
+    python -m paper_2506_11209_amd.trace [--workload NAME] [--point TMxTNxTKxSxNPxNC[xSPLIT]] [--wgs 4]
         [--warmup 20]
 
 For each traced workgroup and K-iteration q the kernel stamps (shader clock):
@@ -30,11 +30,12 @@ def run_traced(wl, point, wgs=4, Ad=None, Bd=None, load_path="registers", warmup
     import torch
     from paper_2506_11209_amd import inputs
     from paper_2506_11209_amd import wsgemm as w
-    tm, tn, tk, stages, np_, nc = point
+    from paper_2506_11209_amd.workloads import unpack
+    tm, tn, tk, stages, np_, nc, split = unpack(point)
     if Ad is None:
         A, B = inputs.make_operands(wl.M, wl.N, wl.K, wl.dtype, wl.dist, wl.seed)
         Ad, Bd = A.cuda(), B.cuda()
-    g = w.WsGemm(wl.M, wl.N, wl.K, (tm, tn, tk), stages, np_, nc, wl.dtype, load_path)
+    g = w.WsGemm(wl.M, wl.N, wl.K, (tm, tn, tk), stages, np_, nc, wl.dtype, load_path, split=split)
     try:
         wgs = min(wgs, g.info.grid)
         iters = g.info.rounds * g.info.iters
@@ -121,7 +122,8 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=20, help="untraced launches before the traced one")
     a = ap.parse_args(argv)
     wl = WORKLOADS[a.workload]
-    point = tuple(int(x) for x in a.point.split("x"))
+    from paper_2506_11209_amd.workloads import parse_point
+    point = parse_point(a.point)
     rec, plan, _ = run_traced(wl, point, a.wgs, load_path=a.load_path, warmup=a.warmup)
     if a.dump:
         np.save(a.dump, rec)

@@ -51,7 +51,7 @@ class ws_gemm_config(ctypes.Structure):
     _fields_ = [("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32), ("tile_k", ctypes.c_int32),
                 ("producer_waves", ctypes.c_int32), ("consumer_waves", ctypes.c_int32),
                 ("stages", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("load_path", ctypes.c_int32)]
+                ("load_path", ctypes.c_int32), ("split", ctypes.c_int32)]
 
 
 class ws_gemm_plan_info(ctypes.Structure):
@@ -123,6 +123,9 @@ _lib.ws_gemm_run.argtypes = [_h, _p, _p, _p, _p]
 _lib.ws_gemm_run.restype = _i32
 _lib.ws_gemm_sync_status.argtypes = [_h, _p]
 _lib.ws_gemm_sync_status.restype = _i32
+_u64p = ctypes.POINTER(ctypes.c_uint64)
+_lib.ws_gemm_clock.argtypes = [_h, _p, _u64p, _u64p, ctypes.POINTER(_i64)]
+_lib.ws_gemm_clock.restype = _i32
 _lib.ws_gemm_query.argtypes = [_h, ctypes.POINTER(ws_gemm_plan_info)]
 _lib.ws_gemm_query.restype = _i32
 _lib.ws_gemm_set_debug.argtypes = [_h, ctypes.POINTER(ws_gemm_debug)]
@@ -153,10 +156,11 @@ def library() -> ctypes.CDLL:
 
 
 def config(tile=(128, 128, 32), stages=3, producer_waves=4, consumer_waves=4, dtype="bf16",
-           load_path="registers"):
+           load_path="registers", split=0):
+    """split: DMA warps per MATH warp (1 or 2); 0 derives it from the wave counts."""
     tm, tn, tk = tile
     return ws_gemm_config(tm, tn, tk, producer_waves, consumer_waves, stages, DTYPE_CODES[dtype],
-                          LOAD_PATHS[load_path])
+                          LOAD_PATHS[load_path], split)
 
 
 # -- C names -----------------------------------------------------------------
@@ -205,6 +209,13 @@ def ws_gemm_sync_status(h, stream_ptr: int = 0) -> int:
     return _lib.ws_gemm_sync_status(h, _p(stream_ptr))
 
 
+def ws_gemm_clock(h, stream_ptr: int = 0):
+    """(status, shader_cycles, ref_ticks, launches); clears the accumulators."""
+    c, r, n = ctypes.c_uint64(0), ctypes.c_uint64(0), _i64(0)
+    s = _lib.ws_gemm_clock(h, _p(stream_ptr), ctypes.byref(c), ctypes.byref(r), ctypes.byref(n))
+    return s, c.value, r.value, n.value
+
+
 def ws_gemm_query(h):
     info = ws_gemm_plan_info()
     s = _lib.ws_gemm_query(h, ctypes.byref(info))
@@ -240,13 +251,14 @@ class WsGemm:
     """A created plan for one (M, N, K, configuration); call it on torch tensors."""
 
     def __init__(self, M, N, K, tile=(128, 128, 32), stages=3, producer_waves=4,
-                 consumer_waves=4, dtype="bf16", load_path="registers", calibration=None):
+                 consumer_waves=4, dtype="bf16", load_path="registers", calibration=None, split=0):
         """calibration: None for the GEMM, else a key of CALIB_KINDS (the
-        calibration kernels of the performance model, same launch)."""
+        calibration kernels of the performance model, same launch).  split:
+        DMA warps per MATH warp (1 or 2; 0 derives it from the wave counts)."""
         self.M, self.N, self.K = M, N, K
         self.dtype = dtype
         self.out_dtype = "f32"
-        self.cfg = config(tile, stages, producer_waves, consumer_waves, dtype, load_path)
+        self.cfg = config(tile, stages, producer_waves, consumer_waves, dtype, load_path, split)
         if calibration is None:
             s, self._h = ws_gemm_create(M, N, K, self.cfg)
             where = "ws_gemm_create"
@@ -300,6 +312,16 @@ class WsGemm:
         import torch
         st = stream if stream is not None else torch.cuda.current_stream()
         return ws_gemm_sync_status(self._h, st.cuda_stream)
+
+    def clock_mhz(self, stream=None):
+        """Average shader clock (MHz) of the launches since the last call, and
+        their count (see ws_gemm_clock); (None, 0) when none took part."""
+        import torch
+        st = stream if stream is not None else torch.cuda.current_stream()
+        s, cyc, ticks, n = ws_gemm_clock(self._h, st.cuda_stream)
+        if s != WS_OK:
+            raise WsGemmError("ws_gemm_clock", s)
+        return (100.0 * cyc / ticks if ticks else None), n
 
     def set_debug(self, spin_limit=0, producer_delay=0, consumer_delay=0):
         s = ws_gemm_set_debug(self._h, ws_gemm_debug(spin_limit, producer_delay, consumer_delay))

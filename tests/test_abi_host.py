@@ -5,7 +5,7 @@ import re
 import pytest
 
 from paper_2506_11209_amd import wsgemm as w
-from paper_2506_11209_amd.workloads import WORKLOADS
+from paper_2506_11209_amd.workloads import WORKLOADS, split_of, unpack
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 GOLDEN = os.path.join(ROOT, "tests", "golden")
@@ -32,7 +32,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_text():
-    assert w.ws_gemm_abi_version() == 6
+    assert w.ws_gemm_abi_version() == 7
     for s in range(7):
         assert w.ws_gemm_status_str(s) and w.ws_gemm_status_str(s) != "unknown status"
     assert w.ws_gemm_status_str(99) == "unknown status"
@@ -54,8 +54,11 @@ def test_plan_headline_shape():
 @pytest.mark.parametrize("name", sorted(WORKLOADS))
 def test_plan_every_workload_point(name):
     wl = WORKLOADS[name]
-    for (tm, tn, tk, stages, np_, nc) in wl.points:
-        s, info = w.ws_gemm_plan(wl.M, wl.N, wl.K, cfg((tm, tn, tk), stages, np_, nc, wl.dtype), 256, 1)
+    for pt in wl.points:
+        tm, tn, tk, stages, np_, nc, split = unpack(pt)
+        c = cfg((tm, tn, tk), stages, np_, nc, wl.dtype)
+        c.split = split
+        s, info = w.ws_gemm_plan(wl.M, wl.N, wl.K, c, 256, 1)
         stage = 2 * (tm * tk + tk * tn)
         if 256 + stages * stage > 163840:
             assert s == w.WS_ERR_LDS_OVERFLOW
@@ -65,7 +68,7 @@ def test_plan_every_workload_point(name):
         assert info.tiles == tiles and info.iters == wl.K // tk
         assert info.grid == min(tiles, 256)
         assert info.rounds == -(-tiles // info.grid)
-        assert info.split == np_ // nc and info.block == 64 * (np_ + nc)
+        assert info.split == split_of(pt) and info.block == 64 * (np_ + nc)
 
 
 def test_lds_overflow_case_from_the_sweep():
@@ -95,11 +98,32 @@ def test_plan_rejections(M, N, K, tile, status):
 
 @pytest.mark.parametrize("np_,nc,stages,status", [
     (3, 4, 3, w.WS_ERR_UNSUPPORTED), (4, 2, 3, w.WS_ERR_UNSUPPORTED), (4, 4, 1, w.WS_ERR_INVALID_ARG),
-    (4, 4, 9, w.WS_ERR_INVALID_ARG), (16, 4, 2, w.WS_ERR_UNSUPPORTED),
+    (4, 4, 9, w.WS_ERR_INVALID_ARG), (16, 4, 2, w.WS_ERR_UNSUPPORTED), (8, 8, 2, w.WS_ERR_UNSUPPORTED),
+    (2, 8, 2, w.WS_ERR_UNSUPPORTED),
 ])
 def test_plan_rejects_wave_and_stage_counts(np_, nc, stages, status):
     s, _ = w.ws_gemm_plan(4096, 4096, 4096, cfg((128, 128, 32), stages, np_, nc), 256, 1)
     assert s == status
+
+
+@pytest.mark.parametrize("np_,nc,split,want", [
+    (4, 4, 0, 1), (8, 4, 0, 2), (4, 4, 1, 1), (4, 4, 2, 2), (8, 4, 2, 2), (1, 1, 0, 1), (2, 1, 0, 2),
+    (4, 8, 0, 1), (4, 8, 1, 1), (4, 8, 2, 2),
+    (8, 4, 1, None), (1, 1, 2, None), (2, 1, 1, None), (0, 4, 1, None), (4, 4, 3, "invalid"),
+])
+def test_plan_split_of_each_arrangement(np_, nc, split, want):
+    """split 0 derives the arrangement from the wave counts; an explicit one
+    must be an arrangement some kernel has."""
+    tile = (256, 256, 64) if nc == 8 else (128, 128, 64) if nc == 4 else (64, 64, 64)
+    c = cfg(tile, 2, np_, nc)
+    c.split = split
+    s, info = w.ws_gemm_plan(4096, 4096, 4096, c, 256, 1)
+    if want == "invalid":
+        assert s == w.WS_ERR_INVALID_ARG
+    elif want is None:
+        assert s == w.WS_ERR_UNSUPPORTED
+    else:
+        assert s == w.WS_OK and info.split == want and info.block == 64 * (np_ + nc)
 
 
 def test_plan_bad_dtype_and_cus():

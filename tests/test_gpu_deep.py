@@ -1,11 +1,14 @@
-"""The deep-prefetch consumer (generated asm K loop, ws_deep_loop.inc) in every
-configuration that runs it (the generator's list: one and two producer
-groups, TK = 64 and 32): its prologue, loop bodies and last four k-steps
-(1-8 K-iterations per tile; TK = 32 tiles with an odd count take the
-compiler-scheduled consumer instead), slot wrap-around at every ring depth
-that fits, two output tiles per workgroup, both producer load paths, the
-polling path (late producers), the consumer delay hook and the watchdog.
-(The general variant keeps the compiler-scheduled consumer.)
+"""The generated asm K loops (ws_deep_loop.inc) in every configuration that
+runs them: the deep-prefetch consumer of four consumer waves (the
+generator's list: four or eight producer waves, one or two producer groups,
+TK = 64 and 32) and the register-lean loop of eight consumer waves (256 x 256
+tiles, four producer waves in one or two groups).  Their prologue, loop
+bodies and last k-steps (1-8 K-iterations per tile; TK = 32 deep-consumer
+tiles with an odd count take the compiler-scheduled consumer instead), slot
+wrap-around at every ring depth that fits, two output tiles per workgroup,
+both producer load paths, the polling path (late producers), the consumer
+delay hook and the watchdog.  (The general variant keeps the
+compiler-scheduled consumers.)
 
 Operands are small integers, so every product is exact: C is compared with
 the oracle on sampled rows and, over all of C, by an exact checksum
@@ -31,7 +34,15 @@ sys.path.insert(0, os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(
 import gen_deep_loop  # noqa: E402  (the list of deep-consumer configurations)
 
 LDS_LIMIT = 163840
-CONFIGS = [(tm, tn, tk, split) for (tm, tn, tk, nc, split) in gen_deep_loop.CONFIGS]
+# (tm, tn, tk, consumer waves, producer waves, split)
+CONFIGS = ([(tm, tn, tk, nc, np_, split) for (tm, tn, tk, nc, np_) in gen_deep_loop.CONFIGS
+            for split in ((1, 2) if np_ == 4 else (2,))] +
+           [(tm, tn, tk, nc, np_, split) for (tm, tn, tk, nc, np_) in gen_deep_loop.ROLL_CONFIGS
+            for split in (1, 2)])
+
+
+def cfg_id(t):
+    return "%dx%dx%d-nc%d-np%d-%d:1" % t
 
 
 def max_stages(tile):
@@ -47,9 +58,11 @@ def exact_checksum(C, A, B, seed):
     return np.array_equal(C.astype(np.float64) @ x, Af @ (Bf @ x))
 
 
-def run_and_check(M, N, K, tile, stages, dtype="bf16", load_path="registers", debug=None, seed=0, split=1):
+def run_and_check(M, N, K, tile, stages, dtype="bf16", load_path="registers", debug=None, seed=0, split=1,
+                  nc=4, np_=None):
     A, B = inputs.make_operands(M, N, K, dtype, "int4", seed)
-    g = w.WsGemm(M, N, K, tile, stages, 4 * split, 4, dtype, load_path)
+    np_ = 4 * split if np_ is None else np_
+    g = w.WsGemm(M, N, K, tile, stages, np_, nc, dtype, load_path, split=split)
     try:
         info = g.info.as_dict()
         if debug:
@@ -71,23 +84,24 @@ def run_and_check(M, N, K, tile, stages, dtype="bf16", load_path="registers", de
 
 @pytest.mark.parametrize("load_path", ["registers", "dma"])
 @pytest.mark.parametrize("iters", [1, 2, 3, 4, 7, 8])
-@pytest.mark.parametrize("cfg", CONFIGS, ids=lambda t: "%dx%dx%d-%d:1" % t)
+@pytest.mark.parametrize("cfg", CONFIGS, ids=cfg_id)
 def test_k_iterations_and_ring_depths(cfg, iters, load_path):
-    tm, tn, tk, split = cfg
+    tm, tn, tk, nc, np_, split = cfg
     tile = (tm, tn, tk)
     M, N, K = 16 * tm, 32 * tn, iters * tk  # 512 tiles: two or more per workgroup
     for stages in range(2, min(4, max_stages(tile)) + 1):
-        log("case deep %s %d:1 S=%d P=%d %s" % (tile, split, iters, stages, load_path))
-        info = run_and_check(M, N, K, tile, stages, load_path=load_path, seed=100 * iters + stages, split=split)
-        assert info["iters"] == iters and info["general"] == 0  # the plain kernel: deep consumer
+        log("case deep %s nc=%d np=%d %d:1 S=%d P=%d %s" % (tile, nc, np_, split, iters, stages, load_path))
+        info = run_and_check(M, N, K, tile, stages, load_path=load_path, seed=100 * iters + stages,
+                             split=split, nc=nc, np_=np_)
+        assert info["iters"] == iters and info["general"] == 0  # the plain kernel: generated loop
         assert info["tiles"] > info["grid"], "each workgroup must take more than one tile"
 
 
-@pytest.mark.parametrize("cfg", CONFIGS, ids=lambda t: "%dx%dx%d-%d:1" % t)
+@pytest.mark.parametrize("cfg", CONFIGS, ids=cfg_id)
 def test_f16(cfg):
-    tm, tn, tk, split = cfg
-    log("case deep f16 %s %d:1" % ((tm, tn, tk), split))
-    run_and_check(8 * tm, 8 * tn, 640, (tm, tn, tk), 2, dtype="f16", seed=7, split=split)
+    tm, tn, tk, nc, np_, split = cfg
+    log("case deep f16 %s nc=%d np=%d %d:1" % ((tm, tn, tk), nc, np_, split))
+    run_and_check(8 * tm, 8 * tn, 640, (tm, tn, tk), 2, dtype="f16", seed=7, split=split, nc=nc, np_=np_)
 
 
 @pytest.mark.parametrize("pdelay,cdelay", [(3, 0), (0, 3), (2, 2)])
@@ -95,6 +109,33 @@ def test_late_producers_and_consumer_delay(pdelay, cdelay):
     # late producers make the consumer's peek come up short, so it polls
     log("case deep delays p=%d c=%d" % (pdelay, cdelay))
     run_and_check(1024, 512, 768, (256, 128, 64), 3, debug=(0, pdelay, cdelay), seed=13)
+
+
+@pytest.mark.parametrize("split", [1, 2])
+@pytest.mark.parametrize("pdelay,cdelay", [(3, 0), (0, 3), (2, 2)])
+def test_late_producers_and_consumer_delay_eight_consumers(pdelay, cdelay, split):
+    log("case roll delays p=%d c=%d split=%d" % (pdelay, cdelay, split))
+    run_and_check(1024, 512, 768, (256, 256, 64), 2, debug=(0, pdelay, cdelay), seed=14, split=split,
+                  nc=8, np_=4)
+
+
+def test_watchdog_eight_consumers():
+    A, B = inputs.make_operands(1024, 512, 1024, "bf16", "int4", 18)
+    log("case roll watchdog")
+    g = w.WsGemm(1024, 512, 1024, (256, 256, 64), 2, 4, 8, "bf16")
+    try:
+        Ad, Bd = A.cuda(), B.cuda()
+        g.set_debug(1, 20, 0)  # one poll allowed, producers ~160k cycles late
+        g(Ad, Bd)
+        assert g.sync_status() == w.WS_ERR_TIMEOUT
+        assert g.sync_status() == w.WS_OK
+        g.set_debug(0, 0, 0)
+        C = g(Ad, Bd)
+        assert g.sync_status() == w.WS_OK
+        Cref, _ = oracle.gemm(inputs.bits(A), inputs.bits(B), "bf16", with_abs=False)
+        assert compare_exact(C.cpu().numpy(), Cref)["ok"]
+    finally:
+        g.close()
 
 
 def test_watchdog_reports_timeout_then_recovers():

@@ -20,15 +20,15 @@ pytestmark = pytest.mark.gpu
 GUARD = 512
 SENTINEL = -7.0
 TORCH_OUT = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
-CONFIGS = sorted({(tm, tn, tk, nc, split, bf16)
-                  for (tm, tn, tk, nc, split, bf16, trace, mode, general) in instances()
-                  if split > 0 and mode == MODE_GEMM and not trace})
-N_CASES = 320
+CONFIGS = sorted({(tm, tn, tk, nc, np_, split, bf16)
+                  for (tm, tn, tk, nc, np_, split, bf16, trace, mode, general) in instances()
+                  if np_ > 0 and mode == MODE_GEMM and not trace})
+N_CASES = 400
 
 
 def draw_case(i):
     rng = np.random.default_rng(7000 + i)
-    tm, tn, tk, nc, split, bf16 = CONFIGS[i % len(CONFIGS)]
+    tm, tn, tk, nc, np_, split, bf16 = CONFIGS[i % len(CONFIGS)]
     dtype = "bf16" if bf16 else "f16"
     if rng.random() < 0.3:  # whole tiles
         M, N, K = (int(rng.integers(1, 4)) * tm, int(rng.integers(1, 4)) * tn, int(rng.integers(1, 5)) * tk)
@@ -44,8 +44,8 @@ def draw_case(i):
     else:
         epi = (float(rng.choice([1.0, 0.5, -2.0, 0.25])), float(rng.choice([0.0, 1.0, -0.5, 2.0])),
                str(rng.choice(["f32", "bf16", "f16"])))
-    return dict(M=M, N=N, K=K, tile=(tm, tn, tk), stages=stages, np_=nc * split, nc=nc, dtype=dtype,
-                load_path=load_path, epi=epi, seed=8000 + i)
+    return dict(M=M, N=N, K=K, tile=(tm, tn, tk), stages=stages, np_=np_, nc=nc, split=split,
+                dtype=dtype, load_path=load_path, epi=epi, seed=8000 + i)
 
 
 @pytest.mark.parametrize("i", range(N_CASES))
@@ -56,7 +56,8 @@ def test_random_case_is_exact(i):
     alpha, beta, out = c["epi"]
     A, B = inputs.make_operands(M, N, K, c["dtype"], "int4", c["seed"])
     C_in = inputs.make_output(M, N, out, "int4", c["seed"] + 1)
-    g = w.WsGemm(M, N, K, c["tile"], c["stages"], c["np_"], c["nc"], c["dtype"], c["load_path"])
+    g = w.WsGemm(M, N, K, c["tile"], c["stages"], c["np_"], c["nc"], c["dtype"], c["load_path"],
+                 split=c["split"])
     try:
         g.set_epilogue(alpha, beta, out)
         buf = torch.full((M * N + GUARD,), SENTINEL, dtype=TORCH_OUT[out])
@@ -76,7 +77,7 @@ def test_random_case_is_exact(i):
 
 
 SYNC_CONFIGS = sorted({(tm, tn, tk, nc, bf16)
-                       for (tm, tn, tk, nc, split, bf16, trace, mode, general) in instances() if split == 0})
+                       for (tm, tn, tk, nc, np_, split, bf16, trace, mode, general) in instances() if np_ == 0})
 N_SYNC_CASES = 2 * len(SYNC_CONFIGS)
 
 

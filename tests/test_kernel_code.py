@@ -17,10 +17,10 @@ pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="library not bui
 
 def test_every_compiled_gemm_kernel_has_a_fingerprint():
     seen = {}
-    for (tm, tn, tk, nc, split, bf16, trace, mode, general) in instances():
-        if split == 0:
+    for (tm, tn, tk, nc, np_, split, bf16, trace, mode, general) in instances():
+        if np_ == 0:
             continue  # the synchronous kernel is another template
-        sym = kc.gemm_symbol(tm, tn, tk, nc, split, bool(bf16), bool(trace), mode, bool(general))
+        sym = kc.gemm_symbol(tm, tn, tk, nc, np_, split, bool(bf16), bool(trace), mode, bool(general))
         fp = kc.kernel_fingerprint(sym, LIB)
         assert len(fp) == 16
         seen[sym] = fp
@@ -29,10 +29,10 @@ def test_every_compiled_gemm_kernel_has_a_fingerprint():
 
 
 def test_fingerprint_is_repeatable_and_unknown_kernels_raise():
-    sym = kc.gemm_symbol(256, 128, 64, 4, 1)
+    sym = kc.gemm_symbol(256, 128, 64, 4, 4, 1)
     assert kc.kernel_fingerprint(sym, LIB) == kc.kernel_fingerprint(sym, LIB)
     with pytest.raises(LookupError):
-        kc.kernel_fingerprint(kc.gemm_symbol(256, 128, 64, 4, 1, mode=MODE_GEMM + 99), LIB)
+        kc.kernel_fingerprint(kc.gemm_symbol(256, 128, 64, 4, 4, 1, mode=MODE_GEMM + 99), LIB)
 
 
 def test_traffic_record_matches_only_its_own_kernel(tmp_path, monkeypatch):
