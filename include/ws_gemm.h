@@ -251,6 +251,32 @@ typedef enum {
 ws_status ws_gemm_create_calibration(int64_t M, int64_t N, int64_t K, const ws_gemm_config* cfg,
                                      int32_t kind, ws_gemm_t* out);
 
+/* C = A B in one call that allocates nothing, for callers that cannot
+ * allocate device or host memory while they run: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  It
+ * validates and plans (M, N, K, cfg) as ws_gemm_create does, picks the same
+ * kernel and launch (the general variant for shapes the tiles do not
+ * divide; default epilogue, fp32 C) and enqueues it on `stream`, with no
+ * handle, no hipMalloc / hipFree and no other allocating call.
+ *
+ * Scratch: the kernels' only device memory beyond A, B and C is the wait
+ * watchdog's word.  Here it lives in a static 256-byte array of the library,
+ * one copy per GPU (looked up on the first call on each device, with that
+ * device current, and held until the process ends).  The kernels write it
+ * only when a wait gives up; this entry point does not report that (use
+ * ws_gemm_create / ws_gemm_run / ws_gemm_sync_status for the watchdog): such
+ * a run exits early and leaves C incomplete.  The scratch need is fixed, so
+ * no problem size is refused for it; sizes are limited as for
+ * ws_gemm_create.  Calls that overlap on one GPU share that GPU's word.
+ *
+ * Arguments as for ws_gemm_create and ws_gemm_run (A, B 16-byte aligned
+ * device pointers, C 4-byte aligned; those an empty problem does not use
+ * may be NULL); `stream` 0 means the current device's null stream.
+ * Asynchronous: returns once the launch is enqueued.  Errors as for those
+ * two calls. */
+ws_status ws_gemm_run_noalloc(int64_t M, int64_t N, int64_t K, const ws_gemm_config* cfg,
+                              const void* A, const void* B, float* C, hipStream_t stream);
+
 /* Free the handle; NULL is a no-op.  Must not race with runs using it. */
 ws_status ws_gemm_destroy(ws_gemm_t h);
 

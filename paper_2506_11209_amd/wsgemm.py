@@ -134,6 +134,8 @@ _lib.ws_gemm_set_epilogue.argtypes = [_h, ctypes.POINTER(ws_gemm_epilogue)]
 _lib.ws_gemm_set_epilogue.restype = _i32
 _lib.ws_gemm_set_trace.argtypes = [_h, _p, _i64, _i32, _i32]
 _lib.ws_gemm_set_trace.restype = _i32
+_lib.ws_gemm_run_noalloc.argtypes = [_i64, _i64, _i64, ctypes.POINTER(ws_gemm_config), _p, _p, _p, _p]
+_lib.ws_gemm_run_noalloc.restype = _i32
 _lib.ws_gemm_destroy.argtypes = [_h]
 _lib.ws_gemm_destroy.restype = _i32
 _lib.ws_model_predict.argtypes = [_i64, _i64, _i64, _i32, _i32, _i32, _i32, _i32,
@@ -232,6 +234,12 @@ def ws_gemm_set_epilogue(h, epi: ws_gemm_epilogue | None) -> int:
 
 def ws_gemm_set_trace(h, buf_ptr: int | None, nbytes: int = 0, wgs: int = 0, iters: int = 0) -> int:
     return _lib.ws_gemm_set_trace(h, _p(buf_ptr) if buf_ptr else None, nbytes, wgs, iters)
+
+
+def ws_gemm_run_noalloc(M, N, K, cfg: ws_gemm_config, A_ptr: int, B_ptr: int, C_ptr: int,
+                        stream_ptr: int = 0) -> int:
+    return _lib.ws_gemm_run_noalloc(M, N, K, ctypes.byref(cfg), _p(A_ptr), _p(B_ptr), _p(C_ptr),
+                                    _p(stream_ptr))
 
 
 def ws_gemm_destroy(h) -> int:
