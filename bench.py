@@ -28,7 +28,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 WORKLOAD = "gemm_8192x8192x8192_bf16_normal"
-DEFAULT_POINT = (256, 128, 64, 3, 4, 4)   # (TM, TN, TK, stages, producer waves, consumer waves)
+# (TM, TN, TK, stages, producer waves, consumer waves, split): 256 x 256 tiles,
+# eight consumer waves (two per SIMD) and four producer waves in one group (1:1)
+DEFAULT_POINT = (256, 256, 64, 2, 4, 8, 1)
 DEFAULT_LOAD_PATH = "registers"
 PEAK_TFLOPS = 2500.0                      # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBS = 8000.0                     # MI355X HBM3E
@@ -134,6 +136,10 @@ def main():
     ap.add_argument("--load-path", default=DEFAULT_LOAD_PATH, choices=("registers", "dma"))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", default=WORKLOAD)
+    ap.add_argument("--cold-flush-mib", type=int, default=0,
+                    help="write a buffer of this many MiB before every timed launch (outside its events), "
+                         "so each launch starts with its operands out of the caches; the roofline entry "
+                         "then comes from the launch events alone")
     ap.add_argument("--min-warmup-s", type=float, default=0.5,
                     help="warm up for at least this long, and until two batches of 10 agree within 1%%")
     a = ap.parse_args()
@@ -174,8 +180,15 @@ def main():
 
     # warm up by count and by time (the clock ramps over the first launches);
     # the launch clock accumulators are cleared just before the timed region
+    flush = None
+    if a.cold_flush_mib > 0:
+        junk = torch.empty(a.cold_flush_mib << 18, dtype=torch.float32, device="cuda")
+
+        def flush():
+            junk.fill_(1.0)
     dev, wall_ms, wu = time_launches(step, a.steps, a.warmup, min_warmup_s=a.min_warmup_s,
-                                     with_warmup=True, before_timed=lambda: g.clock_mhz(stream))
+                                     with_warmup=True, before_timed=lambda: g.clock_mhz(stream),
+                                     between=flush)
     clock_mhz, clock_n = g.clock_mhz(stream)
     st = g.sync_status(stream)
     if st != w.WS_OK:
@@ -228,6 +241,8 @@ def main():
                                        if clock_mhz and bound == "mfma" else None)},
         "warmup_record": wu,
     }
+    if a.cold_flush_mib > 0:
+        out["cold_flush_mib"] = a.cold_flush_mib  # value includes the flushes; roofline does not
     g.close()
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl)

@@ -1,7 +1,7 @@
 """Summaries of rocprofv3 result databases (rocpd SQLite) as short text.
 
     python -m paper_2506_11209_amd.profsummary trace  DB [--kernel SUBSTR] [--skip N]
-    python -m paper_2506_11209_amd.profsummary counters DB [--kernel SUBSTR]
+    python -m paper_2506_11209_amd.profsummary counters DB [--kernel SUBSTR] [--group G --points JSONL]
     python -m paper_2506_11209_amd.profsummary traffic FETCH_DB WRITE_DB CAL_FETCH_DB CAL_WRITE_DB \
         --kernel SUBSTR --point KEY [--workload NAME] [--dtype bf16] [--copy-mib 1024]
 
@@ -59,6 +59,28 @@ def counter_means(db_path: str, kernel: str | None = None):
     return {k: (statistics.fmean(v), len(v)) for k, v in agg.items()}
 
 
+def counter_runs(db_path: str, kernel: str | None, group: int, skip: int = 0):
+    """Matching dispatches in launch order, cut into consecutive runs of
+    `group` (one per case of a program that runs its cases one after another,
+    each `group` times); per run: (kernel name, {counter: mean over the run's
+    dispatches after its first `skip`}, instances summed per dispatch)."""
+    db = sqlite3.connect(db_path)
+    rows = db.execute("select name, dispatch_id, counter_name, counter_value from pmc_events").fetchall()
+    per = collections.defaultdict(float)
+    names = {}
+    for name, did, cn, cv in rows:
+        if kernel is None or kernel in name:
+            per[(did, cn)] += cv
+            names[did] = name
+    dids = sorted(names)
+    out = []
+    for i in range(0, len(dids), group):
+        run = dids[i:i + group][skip:]
+        counters = sorted({cn for (d, cn) in per if d in run})
+        out.append((names[dids[i]], {cn: statistics.fmean(per[(d, cn)] for d in run) for cn in counters}))
+    return out
+
+
 def _mean_counter(db_path, name_part, counter):
     vals = [v for (n, cn), (v, _) in counter_means(db_path).items() if name_part in n and cn == counter]
     if not vals:
@@ -97,7 +119,9 @@ def main(argv=None):
     ap.add_argument("--workload", default=None, help="traffic: workload the counters ran (default: the bench's)")
     ap.add_argument("--dtype", default="bf16", help="traffic: operand dtype of the kernel")
     ap.add_argument("--skip", type=int, default=0, help="trace: leading dispatches per kernel (or run) to drop")
-    ap.add_argument("--group", type=int, default=0, help="trace: dispatches per consecutive run")
+    ap.add_argument("--group", type=int, default=0, help="trace / counters: dispatches per consecutive run")
+    ap.add_argument("--points", default=None,
+                    help="counters --group: the sweep's JSON lines, to label each run with its launch point")
     a = ap.parse_args(argv)
     if a.mode == "traffic":
         traffic(*a.db[:4], a.kernel, a.point, a.copy_mib, a.workload, a.dtype)
@@ -112,6 +136,15 @@ def main(argv=None):
         for name, d in sorted(kernel_durations(a.db, a.kernel, a.skip).items(), key=lambda x: -sum(x[1])):
             print("%-72s calls=%-5d mean_us=%.2f median_us=%.2f min_us=%.2f" % (
                 name[:72], len(d), statistics.fmean(d), statistics.median(d), min(d)))
+    elif a.group > 0:
+        import json
+        labels = []
+        if a.points:
+            with open(a.points) as f:
+                labels = [r["point"] for r in map(json.loads, f) if r.get("status") == "ok"]
+        for i, (name, c) in enumerate(counter_runs(a.db, a.kernel, a.group, a.skip)):
+            label = labels[i] if i < len(labels) else "run %d" % i
+            print(json.dumps({"point": label, "kernel": name, "counters": c}))
     else:
         for (name, cn), (mean, n) in sorted(counter_means(a.db, a.kernel).items()):
             print("%-72s %-32s mean=%.6g dispatches=%d" % (name[:72], cn, mean, n))

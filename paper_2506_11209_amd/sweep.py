@@ -89,7 +89,10 @@ def main(argv=None):
     ap.add_argument("--load-paths", default="registers,dma",
                     help="comma-separated producer load paths to sweep (registers, dma)")
     ap.add_argument("--points", default=None,
-                    help="comma-separated TMxTNxTKxSTAGESxNPxNC list (default: the workload's)")
+                    help="comma-separated TMxTNxTKxSTAGESxNPxNC[xSPLIT] list (default: the workload's)")
+    ap.add_argument("--min-warmup-s", type=float, default=0.3,
+                    help="warm each point up for at least this long (0: exactly --warmup launches, "
+                         "as counter runs need)")
     a = ap.parse_args(argv)
     wl = WORKLOADS[a.workload]
     points = wl.points
@@ -114,7 +117,7 @@ def main(argv=None):
             if key in done:
                 continue
             print("sweep point %s" % key, file=sys.stderr, flush=True)
-            rec = measure_point(wl, p, Ad, Bd, C, a.steps, a.warmup, lp)
+            rec = measure_point(wl, p, Ad, Bd, C, a.steps, a.warmup, lp, a.min_warmup_s)
             line = json.dumps(rec)
             print(line, flush=True)
             if a.out:

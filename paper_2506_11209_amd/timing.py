@@ -50,7 +50,10 @@ def time_launches(launch, steps: int, warmup: int, min_warmup_s: float = 0.0,
     (synchronised both sides), plus the warm-up record if ``with_warmup``.
     With ``min_warmup_s`` > 0 the warm-up is ``warm_up``'s (count, time and
     settled batches); otherwise it is ``warmup`` launches.  ``before_timed()``,
-    if given, runs between the warm-up and the timed region (synchronised)."""
+    if given, runs between the warm-up and the timed region (synchronised).
+    ``between()``, if given, is enqueued before every timed launch, outside
+    its pair of events (a cache flush for cold-cache timing); the wall-clock
+    time per step then includes it."""
     if min_warmup_s > 0:
         wu = warm_up(launch, warmup, min_warmup_s)
     else:
@@ -65,6 +68,8 @@ def time_launches(launch, steps: int, warmup: int, min_warmup_s: float = 0.0,
         torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
+        if between is not None:
+            between()
         starts[i].record()
         launch()
         ends[i].record()

@@ -92,7 +92,7 @@ WORKLOADS = {
                  _sweep_8192()),
         # small integers at the headline size: every element of C is exact
         Workload("gemm_8192x8192x8192_bf16_int4", 8192, 8192, 8192, "bf16", "int4", 33, True,
-                 ((256, 128, 64, 3, 4, 4),)),
+                 ((256, 256, 64, 2, 4, 8, 1), (256, 128, 64, 3, 4, 4))),
         Workload("gemm_16384x256x8192_bf16_uniform", 16384, 256, 8192, "bf16", "uniform", 4, False,
                  ((128, 64, 64, 4, 8, 4),)),
         Workload("gemm_2048x2048x32768_bf16_normal_k", 2048, 2048, 32768, "bf16", "normal_k", 5,
