@@ -44,7 +44,7 @@ def warm_up(launch, min_launches: int, min_seconds: float = 0.5, batch: int = 10
 
 
 def time_launches(launch, steps: int, warmup: int, min_warmup_s: float = 0.0,
-                  with_warmup: bool = False, before_timed=None):
+                  with_warmup: bool = False, before_timed=None, between=None):
     """Warm up, then run ``launch()`` ``steps`` times; return the per-launch
     device ms and the wall-clock ms per step of the timed region
     (synchronised both sides), plus the warm-up record if ``with_warmup``.
