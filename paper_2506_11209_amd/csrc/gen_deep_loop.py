@@ -413,9 +413,19 @@ def _kxor(a, b):
     return 32 * (a ^ b)
 
 
-def program_roll(E: Emitter, c: RollCfg, bf16: bool, S: int | None):
+def program_roll(E: Emitter, c: RollCfg, bf16: bool, S: int | None, traced: bool = False):
     """Emit the roll block (see above).  With S given (a dry run) the loop body
-    is repeated once per K-iteration with absolute k-step numbers in the tags."""
+    is repeated once per K-iteration with absolute k-step numbers in the tags.
+
+    traced: the event-trace twin (consumer wave 0 of traced workgroups).  Per
+    K-iteration u it stores three shader-clock stamps (s_memtime, low 32 bits)
+    into the record of K-iteration tq + u of the trace buffer: the slot seen
+    full (event 4, at the check of u), the MFMAs of u under way (event 5, after
+    its first k-step's first MFMA column) and the slot released (event 6).
+    Each stamp waits for every LDS operation of the wave (the timer is a
+    scalar load and shares their counter); the stamps sit where at most two
+    reads are outstanding, and those two are waited for right after anyway,
+    except at the release."""
     mfma = "v_mfma_f32_32x32x16_bf16" if bf16 else "v_mfma_f32_32x32x16_f16"
     KS = c.ks
     emit = E.emit
@@ -527,22 +537,50 @@ def program_roll(E: Emitter, c: RollCfg, bf16: bool, S: int | None):
         emit("s_cbranch_scc1 5b")
         emit("6:")
 
+    def stamp(ev, ahead_of_ti):
+        # store the low 32 bits of the shader clock as event ev of record
+        # ti + ahead_of_ti (skipped past the buffer's records), from lane 0
+        if not traced:
+            return
+        emit("s_memtime s[100:101]")
+        E.emit("s_waitcnt lgkmcnt(0)")
+        E.ops.clear()  # everything issued so far has completed
+        emit("s_add_u32 %%[t0], %%[ti], %d" % ahead_of_ti)
+        emit("s_cmp_lt_u32 %[t0], %[tlim]")
+        emit("s_cbranch_scc0 7f")
+        emit("s_lshl_b32 %[t1], %[t0], 5")
+        emit("s_add_u32 %%[t1], %%[t1], %d" % (4 * ev))
+        emit("v_mov_b32 %[vx], %[t1]")
+        emit("v_mov_b32 %[vq], s100")
+        emit("s_mov_b64 %[sav], exec")
+        emit("s_mov_b64 exec, 1")
+        emit("global_store_dword %[vx], %[vq], %[tr]")
+        emit("s_mov_b64 exec, %[sav]")
+        emit("s_nop 1")
+        emit("7:")
+
     def kstep(seg, t, ahead):
         # k-step t of the tile; ahead: k-step t + 1 exists (read it now)
         kss = t % KS
         last_of_iter = kss == KS - 1
+        if traced and kss == 0:
+            emit("s_add_u32 %[ti], %[ti], 1")  # K-iteration t / KS of the tile starts
         for mb in range(c.bm):
             E.wait_for((seg, kss, "a", mb), lambda tag, mb=mb: tag == ("A", t, mb) or
                        (mb == 0 and tag == ("B", t, 0)))
             mf(mb, 0)
+        if kss == 0:
+            stamp(5, 0)
         if ahead and last_of_iter:
             enter((seg, kss, "enter"), (t + 1) // KS)
+            stamp(4, 1)
         if ahead:
             read_b(t + 1, 0)
         E.wait_for((seg, kss, "b1"), lambda tag: tag == ("B", t, 1))
         mf(0, 1)
         if last_of_iter:
             release((seg, kss, "rel"), t // KS)
+            stamp(6, 0)
         if ahead:
             emit("v_xor_b32 %%[va], %d, %%[va]" % _kxor(kss, (t + 1) % KS))
             read_a(t + 1, 0)
@@ -561,6 +599,8 @@ def program_roll(E: Emitter, c: RollCfg, bf16: bool, S: int | None):
     emit("s_mov_b32 %[rs], %[slot]")
     emit("s_mov_b32 %[rt], %[ft]")
     emit("s_mov_b32 %[rel], %[slot]")
+    if traced:
+        emit("s_sub_u32 %[ti], %[tq], 1")  # record index of the K-iteration under way
     emit("s_mul_i32 %%[rb], %%[rs], %d" % c.stage)
     emit("s_add_u32 %[rb], %[rb], %[ring]")
     peek(1)
@@ -600,54 +640,69 @@ def program_roll(E: Emitter, c: RollCfg, bf16: bool, S: int | None):
         emit("s_nop 15")
 
 
-def gen_roll_block(c: RollCfg, bf16: bool) -> list[str]:
+def gen_roll_block(c: RollCfg, bf16: bool, traced: bool = False) -> list[str]:
     waits = {}
     for S in (1, 2, 3, 5):
         E = Emitter()
-        program_roll(E, c, bf16, S)
+        program_roll(E, c, bf16, S, traced)
         for site, n in E.need.items():
             waits[site] = min(waits.get(site, LGKM_MAX), n)
     E = Emitter(waits)
-    program_roll(E, c, bf16, None)
+    program_roll(E, c, bf16, None, traced)
     return E.lines
 
 
-def gen_roll_struct(c: RollCfg, bf16: bool) -> str:
-    lines = gen_roll_block(c, bf16)
-    acc_ops = ", ".join('[c%d_%d] "+v"(c[%d][%d])' % (mb, nb, mb, nb) for mb in range(c.bm) for nb in range(c.bn))
-    clobbers = ", ".join('"v%d"' % r for r in range(c.frag_base, c.vgprs))
-    body = "\n".join('        "%s\\n\\t"' % l for l in lines)
-    return """template <>
-struct RollLoop<%(tm)d, %(tn)d, %(tk)d, %(nc)d, %(np)d, %(bf16)s> {
-  static constexpr bool kAvailable = true;
-  // va / vb: this lane's A and B read addresses for k-step 0 of the tile's
-  // first slot (moved along by the block).
-  static __device__ __forceinline__ uint32_t tile(f32x16_t (&c)[%(bm)d][%(bn)d], uint32_t va, uint32_t vb,
+_ROLL_FN = """  static __device__ __forceinline__ uint32_t %(name)s(f32x16_t (&c)[%(bm)d][%(bn)d], uint32_t va, uint32_t vb,
                                                   uint32_t& slot, uint32_t& ftarget, uint32_t P, uint32_t S,
                                                   uint32_t ring, uint32_t fullb, uint32_t emptyb, uint32_t abortb,
-                                                  int32_t lim, int32_t dly) {
+                                                  int32_t lim, int32_t dly%(targs)s) {
 #if defined(__HIP_DEVICE_COMPILE__)
-    uint32_t st, rs, rt, rb, rel, kk, t0, t1, spins, vp, vq, vx;
+    uint32_t st, rs, rt, rb, rel, kk, t0, t1, spins, vp, vq, vx%(tvars)s;
     uint64_t sav;
     asm volatile(
 %(body)s
         : %(acc)s, [slot] "+s"(slot), [ft] "+s"(ftarget), [st] "=&s"(st), [rs] "=&s"(rs), [rt] "=&s"(rt),
           [rb] "=&s"(rb), [rel] "=&s"(rel), [kk] "=&s"(kk), [t0] "=&s"(t0), [t1] "=&s"(t1),
           [spins] "=&s"(spins), [sav] "=&s"(sav), [va] "+v"(va), [vb] "+v"(vb), [vp] "=&v"(vp),
-          [vq] "=&v"(vq), [vx] "=&v"(vx)
+          [vq] "=&v"(vq), [vx] "=&v"(vx)%(touts)s
         : [P] "s"(P), [S] "s"(S), [ring] "s"(ring), [fullb] "s"(fullb), [emptyb] "s"(emptyb),
-          [abortb] "s"(abortb), [lim] "s"(lim), [dly] "s"(dly)
-        : "memory", "scc", %(clobbers)s);
+          [abortb] "s"(abortb), [lim] "s"(lim), [dly] "s"(dly)%(tins)s
+        : "memory", "scc", %(clobbers)s%(tclob)s);
     return st;
 #else
     (void)c; (void)va; (void)vb; (void)slot; (void)ftarget; (void)P; (void)S; (void)ring;
-    (void)fullb; (void)emptyb; (void)abortb; (void)lim; (void)dly;
+    (void)fullb; (void)emptyb; (void)abortb; (void)lim; (void)dly;%(tvoid)s
     return 0;
 #endif
   }
-};
-""" % dict(tm=c.tm, tn=c.tn, tk=c.tk, nc=c.nc, np=c.np, bf16="true" if bf16 else "false", bm=c.bm,
-           bn=c.bn, body=body, acc=acc_ops, clobbers=clobbers)
+"""
+
+
+def gen_roll_struct(c: RollCfg, bf16: bool) -> str:
+    acc_ops = ", ".join('[c%d_%d] "+v"(c[%d][%d])' % (mb, nb, mb, nb) for mb in range(c.bm) for nb in range(c.bn))
+    clobbers = ", ".join('"v%d"' % r for r in range(c.frag_base, c.vgprs))
+    fns = []
+    for traced in (False, True):
+        lines = gen_roll_block(c, bf16, traced)
+        body = "\n".join('        "%s\\n\\t"' % l for l in lines)
+        t = dict(targs="", tvars="", touts="", tins="", tclob="", tvoid="")
+        if traced:
+            t = dict(targs=",\n                                                  uint32_t* trace, uint32_t tq, uint32_t tlim",
+                     tvars=", ti", touts=', [ti] "=&s"(ti)',
+                     tins=', [tr] "s"(trace), [tq] "s"(tq), [tlim] "s"(tlim)', tclob=', "s100", "s101"',
+                     tvoid=" (void)trace; (void)tq; (void)tlim;")
+        fns.append(_ROLL_FN % dict(name="tile_traced" if traced else "tile", bm=c.bm, bn=c.bn, body=body,
+                                   acc=acc_ops, clobbers=clobbers, **t))
+    return """template <>
+struct RollLoop<%(tm)d, %(tn)d, %(tk)d, %(nc)d, %(np)d, %(bf16)s> {
+  static constexpr bool kAvailable = true;
+  // va / vb: this lane's A and B read addresses for k-step 0 of the tile's
+  // first slot (moved along by the block).  tile_traced also stores the
+  // consumer's event stamps of K-iterations tq, tq + 1, ... of the trace
+  // record buffer `trace` (tlim records).
+%(fns)s};
+""" % dict(tm=c.tm, tn=c.tn, tk=c.tk, nc=c.nc, np=c.np, bf16="true" if bf16 else "false",
+           fns="\n".join(fns))
 
 
 def generate() -> str:

@@ -637,12 +637,24 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
   }
 
   const bool tracing = TRACE && args.trace != nullptr && (int)blockIdx.x < args.trace_wgs;
+  // The eight-consumer arrangement's consumer does not copy stamps out of the
+  // LDS header: its producers store their events straight into the record.
+  uint32_t* trec = (tracing && NC == 8) ? args.trace + (size_t)blockIdx.x * args.trace_iters * kTraceEvents
+                                        : nullptr;
+  auto stamp = [&](uint32_t iq, int ev, WSG_LDS uint32_t* hdr, uint32_t value) {
+    if (trec) {
+      if (iq < (uint32_t)args.trace_iters && lane == 0) trec[iq * kTraceEvents + ev] = value;
+    } else {
+      lds_stamp(hdr, value);
+    }
+  };
   // signal(): data of the slot has landed; stamp its landing time first when tracing.
-  auto publish = [&](uint32_t pslot) {
+  auto publish = [&](uint32_t pq) {
+    const uint32_t pslot = ring_slot(pq, (uint32_t)args.stages);
     if (tracing) {
       const uint32_t t = cycles32();
-      if (DO_A && a_rank == 0) lds_stamp(&full[kStampLandA + pslot], t);
-      if (DO_B && b_rank == 0) lds_stamp(&full[kStampLandB + pslot], t);
+      if (DO_A && a_rank == 0) stamp(pq, 2, &full[kStampLandA + pslot], t);
+      if (DO_B && b_rank == 0) stamp(pq, 3, &full[kStampLandB + pslot], t);
     }
     lds_signal(&full[pslot]);
   };
@@ -665,7 +677,7 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
         if ((int32_t)(lds_read_now(&empty[slot]) - need) < 0) {
           while (q_sig < q) {  // publish pending iterations first, oldest first
             wait_landed<LOADS>(q - q_sig - 1);
-            publish(ring_slot(q_sig, P));
+            publish(q_sig);
             ++q_sig;
           }
           if (!wait_counter(&empty[slot], need, abort_flag, args.spin_limit, args.err)) {
@@ -676,7 +688,7 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
       }
       debug_delay(args.producer_delay);
       compiler_fence();
-      if (tracing && a_rank == 0 && DO_A) lds_stamp(&full[kStampIssueA + slot], cycles32());
+      if (tracing && a_rank == 0 && DO_A) stamp(q, 0, &full[kStampIssueA + slot], cycles32());
       WSG_LDS char* a_dst = smem + kHeaderBytes + slot * G::STAGE;
       WSG_LDS char* b_dst = a_dst + G::A_BYTES;
       if constexpr (DO_A) {
@@ -688,7 +700,7 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
                                            16, 0, 0);
       }
       if constexpr (DO_B) {
-        if (tracing && b_rank == 0) lds_stamp(&full[kStampIssueB + slot], cycles32());
+        if (tracing && b_rank == 0) stamp(q, 1, &full[kStampIssueB + slot], cycles32());
         const char* src = (const char*)(b_tile + (int64_t)kk * TK * N);
 #pragma unroll
         for (int n = 0; n < B_PER; ++n)
@@ -699,14 +711,14 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
       // signal(): iteration q - lag has landed once at most `lag` newer ones are in flight.
       if (q + 1 - q_sig > lag) {
         wait_landed<LOADS>(lag);
-        publish(ring_slot(q_sig, P));
+        publish(q_sig);
         ++q_sig;
       }
     }
   }
   while (q_sig < q) {
     wait_landed<LOADS>(q - q_sig - 1);
-    publish(ring_slot(q_sig, P));
+    publish(q_sig);
     ++q_sig;
   }
 }
@@ -763,6 +775,17 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
   const uint32_t lane16 = (uint32_t)lane * 16u;
 
   const bool tracing = TRACE && args.trace != nullptr && (int)blockIdx.x < args.trace_wgs;
+  // The eight-consumer arrangement's consumer does not copy stamps out of the
+  // LDS header: its producers store their events straight into the record.
+  uint32_t* trec = (tracing && NC == 8) ? args.trace + (size_t)blockIdx.x * args.trace_iters * kTraceEvents
+                                        : nullptr;
+  auto stamp = [&](uint32_t iq, int ev, WSG_LDS uint32_t* hdr, uint32_t value) {
+    if (trec) {
+      if (iq < (uint32_t)args.trace_iters && lane == 0) trec[iq * kTraceEvents + ev] = value;
+    } else {
+      lds_stamp(hdr, value);
+    }
+  };
   const int Gd = gridDim.x;
   const int g0 = first_slot(args);
   const int my_tiles = (args.num_tiles - g0 + Gd - 1) / Gd;
@@ -879,12 +902,12 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
       if (tracing) {
         const uint32_t t = cycles32();
         if (DO_A && a_rank == 0) {
-          lds_stamp(&full[kStampIssueA + slot], t_issue[u]);
-          lds_stamp(&full[kStampLandA + slot], t);
+          stamp(q, 0, &full[kStampIssueA + slot], t_issue[u]);
+          stamp(q, 2, &full[kStampLandA + slot], t);
         }
         if (DO_B && b_rank == 0) {
-          lds_stamp(&full[kStampIssueB + slot], t_issue[u]);
-          lds_stamp(&full[kStampLandB + slot], t);
+          stamp(q, 1, &full[kStampIssueB + slot], t_issue[u]);
+          stamp(q, 3, &full[kStampLandB + slot], t);
         }
       }
       lds_signal(&full[slot]);  // waits for the LDS writes, then signals
@@ -1232,7 +1255,7 @@ __device__ __forceinline__ void consumer_deep(const KernelArgs& args, WSG_LDS ch
 // fragments are single-buffered and refilled right after their last MFMA of
 // the k-step; the other consumer wave of the SIMD covers the read latency.
 // ---------------------------------------------------------------------------
-template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, int MODE, bool GENERAL>
+template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
 __device__ __forceinline__ void consumer_roll(const KernelArgs& args, WSG_LDS char* smem, int cw,
                                               int lane) {
   using G = Cfg<TM, TN, TK, NC, NPW, SPLIT, BF16>;
@@ -1265,6 +1288,15 @@ __device__ __forceinline__ void consumer_roll(const KernelArgs& args, WSG_LDS ch
   const uint32_t emptyb = (uint32_t)(uintptr_t)empty;
   const uint32_t abortb = (uint32_t)(uintptr_t)abort_flag;
 
+  // Event trace: consumer wave 0 of the traced workgroups runs the block's
+  // traced twin, which stores events 4-6 of every K-iteration; the first
+  // K-iteration's event 4 and each tile's event 7 are stored here.
+  const bool tracing = TRACE && args.trace != nullptr && cw == 0 && (int)blockIdx.x < args.trace_wgs;
+  uint32_t* trec = tracing ? args.trace + (size_t)blockIdx.x * args.trace_iters * kTraceEvents : nullptr;
+  auto record = [&](uint32_t iq, int ev, uint32_t value) {
+    if (tracing && iq < (uint32_t)args.trace_iters && lane == 0) trec[iq * kTraceEvents + ev] = value;
+  };
+
   int v = g0, ti, tj;
   tile_coords(v, args.tiles_m, args.tiles_n, args.group_m, &ti, &tj);
   f32x16_t acc[BM][BN];
@@ -1275,9 +1307,17 @@ __device__ __forceinline__ void consumer_roll(const KernelArgs& args, WSG_LDS ch
 #pragma unroll
       for (int nb = 0; nb < BN; ++nb) acc[mb][nb] = f32x16_t{};
     if (!wait_counter(&full[slot], ftarget, abort_flag, args.spin_limit, args.err)) return;
+    const uint32_t q0 = (uint32_t)t * S;  // the tile's first K-iteration in this workgroup's sequence
+    if (t == 0) record(q0, 4, cycles32());
     const uint32_t base = ring + slot * (uint32_t)G::STAGE;
-    const uint32_t st = Loop::tile(acc, base + a_off0, base + b_off, slot, ftarget, P, S, ring, fullb,
-                                   emptyb, abortb, args.spin_limit, args.consumer_delay);
+    uint32_t st;
+    if (tracing)
+      st = Loop::tile_traced(acc, base + a_off0, base + b_off, slot, ftarget, P, S, ring, fullb, emptyb,
+                             abortb, args.spin_limit, args.consumer_delay, trec, q0,
+                             (uint32_t)args.trace_iters);
+    else
+      st = Loop::tile(acc, base + a_off0, base + b_off, slot, ftarget, P, S, ring, fullb, emptyb, abortb,
+                      args.spin_limit, args.consumer_delay);
     if (st != 0) {
       if (st == 2) report_timeout(abort_flag, args.err);
       return;
@@ -1286,6 +1326,7 @@ __device__ __forceinline__ void consumer_roll(const KernelArgs& args, WSG_LDS ch
     // never taken: M > 0) without writing C.
     if (MODE != kModeMath || args.M < 0)
       store_tile<TM, TN, G::WM, G::WN, BM, BN, GENERAL, 1>(args, acc, ti, tj, wm, wn, lane);
+    record(q0 + S - 1, 7, cycles32());
     v += Gd;
     tile_coords(v, args.tiles_m, args.tiles_n, args.group_m, &ti, &tj);
   }
@@ -1510,10 +1551,11 @@ __global__ void __launch_bounds__((NC + NPW) * 64) ws_gemm_kernel(KernelArgs arg
       consumer_release_only<G::NP, NC>(args, smem);
     } else if constexpr (MODE == kModeEpilogue) {
       consumer_epilogue_only<TM, TN, TK, NC, NPW, SPLIT, BF16>(args, wave, lane);
-    } else if constexpr (!GENERAL && !TRACE && (MODE == kModeGemm || MODE == kModeMath) &&
+    } else if constexpr (!GENERAL && (MODE == kModeGemm || MODE == kModeMath) &&
                          RollLoop<TM, TN, TK, NC, NPW, BF16>::kAvailable) {
-      // Eight consumer waves: the generated register-lean K loop.
-      consumer_roll<TM, TN, TK, NC, NPW, SPLIT, BF16, MODE, GENERAL>(args, smem, wave, lane);
+      // Eight consumer waves: the generated register-lean K loop (and its
+      // event-traced twin).
+      consumer_roll<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
     } else if constexpr (G::NW > 8 && G::BM * G::BN >= 8) {
       // Three waves per SIMD leave 168 VGPRs: the largest wave tiles then
       // take the single-buffered consumer.

@@ -233,7 +233,8 @@ def test_full_size_workload(name, point, load_path):
 # Event trace: results stay exact, and per K-iteration the stamps are ordered
 # as the protocol requires (issue <= landed <= observed full <= release).
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("point", [(128, 128, 64, 3, 4, 4), (128, 128, 32, 4, 8, 4)])
+@pytest.mark.parametrize("point", [(128, 128, 64, 3, 4, 4), (128, 128, 32, 4, 8, 4), (256, 256, 64, 2, 4, 8, 1),
+                                   (256, 256, 32, 4, 4, 8, 2)])
 def test_trace_is_ordered_and_harmless(point):
     from paper_2506_11209_amd.trace import rel, run_traced
     from paper_2506_11209_amd.workloads import Workload
@@ -248,3 +249,5 @@ def test_trace_is_ordered_and_harmless(point):
     assert np.all(ready >= np.maximum(la, lb))
     assert np.all(relz >= ready)
     assert np.all(np.diff(mma) > 0)
+    if point[5] == 8:  # the generated loop's stamps: full seen, MFMAs under way, released
+        assert np.all(mma >= ready) and np.all(relz >= mma)

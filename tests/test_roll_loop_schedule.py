@@ -37,15 +37,17 @@ HEADER = 256
 
 
 def blocks():
-    """{(tm, tn, tk, nc, np, bf16): [asm lines]} of the RollLoop blocks."""
+    """{(tm, tn, tk, nc, np, bf16, traced): [asm lines]} of the RollLoop blocks
+    (tile and its event-traced twin tile_traced)."""
     with open(gen.OUT) as f:
         text = f.read()
     out = {}
     for m in re.finditer(r"struct RollLoop<(\d+), (\d+), (\d+), (\d+), (\d+), (true|false)> \{(.*?)\n\};", text,
                          re.S):
         key = tuple(int(x) for x in m.groups()[:5]) + (m.group(6) == "true",)
-        lines = re.findall(r'^\s*"(.*)\\n\\t"$', m.group(7), re.M)
-        out[key] = [l.strip() for l in lines]
+        for fn in re.finditer(r"uint32_t (tile|tile_traced)\((.*?)return st;", m.group(7), re.S):
+            lines = re.findall(r'^\s*"(.*)\\n\\t"$', fn.group(2), re.M)
+            out[key + (fn.group(1) == "tile_traced",)] = [l.strip() for l in lines]
     return out
 
 
@@ -118,7 +120,9 @@ class Sim:
         self.errors = []
         ring = HEADER
         self.s = {"slot": slot0, "ft": 4 * (1 + 0), "P": P, "S": S, "ring": ring, "fullb": 0,
-                  "emptyb": 32, "abortb": 64, "lim": 1000, "dly": 0}
+                  "emptyb": 32, "abortb": 64, "lim": 1000, "dly": 0, "tq": 7, "tlim": 1000}
+        self.vx = None
+        self.stores = []          # (record index, event) of the trace stores, in order
         base = ring + slot0 * c.stage
         self.va = [base + ln.a_off0 for ln in lanes]
         self.vb = [base + ln.b_off for ln in lanes]
@@ -281,8 +285,14 @@ class Sim:
             elif op == "v_xor_b32" and args[0] == "%[va]":
                 x = int(args[1])
                 self.va = [v ^ x for v in self.va]
-            elif op in ("v_mov_b32",):
-                pass
+            elif op == "v_mov_b32":
+                if args[0] == "%[vx]" and args[1].startswith("%["):
+                    self.vx = self.val(args[1])
+            elif op == "s_memtime":
+                pass  # waited for by the s_waitcnt lgkmcnt(0) that follows it (checked below)
+            elif op == "global_store_dword":
+                assert args[0] == "%[vx]" and args[2] == "%[tr]", l
+                self.stores.append((self.vx // 32, (self.vx % 32) // 4))
             elif op == "s_mov_b32":
                 s[args[0][2:-1]] = self.val(args[1])
             elif op == "s_mov_b64":
@@ -301,7 +311,7 @@ class Sim:
                 last_cmp = l
                 a, b = self.val(args[0]), self.val(args[1])
                 scc = {"s_cmp_eq_u32": a == b, "s_cmp_lg_u32": a != b, "s_cmp_ge_i32": a >= b,
-                       "s_cmp_gt_i32": a > b, "s_cmp_le_i32": a <= b}[op]
+                       "s_cmp_gt_i32": a > b, "s_cmp_le_i32": a <= b, "s_cmp_lt_u32": a < b}[op]
             elif op in ("s_cbranch_scc0", "s_cbranch_scc1", "s_branch"):
                 ref = args[0]
                 if op == "s_branch":
@@ -348,19 +358,39 @@ def test_roll_block_reads_waits_and_releases(key, S, polls, P):
     c = gen.RollCfg(*key[:5])
     slot0 = 1 % P
     sim = Sim(c, S, polls, lanes_of(c), P, slot0)
-    sim.run(blocks()[key])
+    lines = blocks()[key]
+    sim.run(lines)
     assert not sim.errors, sim.errors[:5]
     assert sim.mfmas == c.bm * c.bn * c.ks * S
     assert sim.released == list(range(S)), sim.released
     assert sim.s["st"] == 0
     assert sim.s["slot"] == (slot0 + S) % P
     assert sim.s["ft"] == 4 * (1 + (slot0 + S) // P)  # np = 4 signals per use of a slot
+    if key[6]:
+        # traced twin: per K-iteration u of the tile, record tq + u gets the
+        # slot-full stamp (event 4, from the second K-iteration on: the caller
+        # stores the first), then MFMAs under way (5), then released (6)
+        tq = sim.s["tq"]
+        want = []
+        for u in range(S):
+            want.append((tq + u, 5))
+            if u + 1 < S:
+                want.append((tq + u + 1, 4))
+            want.append((tq + u, 6))
+        assert sim.stores == want, sim.stores
+        for i, l in enumerate(lines):  # every timer read is waited for at once
+            if l.startswith("s_memtime"):
+                assert lines[i + 1] == "s_waitcnt lgkmcnt(0)"
+    else:
+        assert not sim.stores and not any(l.startswith("s_memtime") for l in lines)
 
 
 def test_generator_covers_the_dispatched_configurations():
     keys = set(blocks())
     for t in gen.ROLL_CONFIGS:
-        assert t + (True,) in keys and t + (False,) in keys
+        for bf16 in (True, False):
+            for traced in (False, True):
+                assert t + (bf16, traced) in keys
 
 
 @pytest.mark.parametrize("key", sorted(blocks()), ids=lambda v: str(v))
@@ -374,6 +404,13 @@ def test_checker_catches_a_weakened_wait(key):
         n = int(re.search(r"\((\d+)\)", l).group(1))
         if n >= 15 or i + 1 == len(lines) or "s_nop" in lines[i + 1]:
             continue
+        if lines[i - 1].startswith("s_memtime"):
+            continue  # the timer's own wait (checked in the main test)
+        j = i - 1
+        while j >= 0 and not lines[j].startswith(("ds_", "s_waitcnt")):
+            j -= 1
+        if j >= 0 and lines[j] == "s_waitcnt lgkmcnt(0)":
+            continue  # nothing issued since a full drain: the wait is already met
         total += 1
         bad = list(lines)
         bad[i] = "s_waitcnt lgkmcnt(%d)" % (n + 1)
