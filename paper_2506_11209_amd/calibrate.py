@@ -66,8 +66,9 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_us(kind, M, N, K, tile, np_, load_path, A, B, C, steps, warmup):
-    g = w.WsGemm(M, N, K, tile, stages_for(tile), np_, 4, "bf16", load_path, calibration=kind)
+def kernel_us(kind, M, N, K, tile, np_, load_path, A, B, C, steps, warmup, nc=4, split=0, stages=None):
+    g = w.WsGemm(M, N, K, tile, stages or stages_for(tile), np_, nc, "bf16", load_path, calibration=kind,
+                 split=split)
     try:
         st = torch.cuda.current_stream().cuda_stream
         a, b, c = A.data_ptr(), B.data_ptr(), C.data_ptr()
@@ -80,11 +81,12 @@ def kernel_us(kind, M, N, K, tile, np_, load_path, A, B, C, steps, warmup):
         g.close()
 
 
-def fixed_costs_us(M, tile, np_, load_path, A, B, C, warmup):
+def fixed_costs_us(M, tile, np_, load_path, A, B, C, warmup, nc=4, split=0, stages=None):
     """Empty-kernel and epilogue-only-kernel times (us) of one launch point
     (medians of FIXED_LAUNCHES launches each) and the launch's rounds."""
-    empty = w.WsGemm(M, M, tile[2], tile, stages_for(tile), np_, 4, "bf16", load_path, calibration="empty")
-    epi = w.WsGemm(M, M, tile[2], tile, stages_for(tile), np_, 4, "bf16", load_path, calibration="epilogue")
+    P = stages or stages_for(tile)
+    empty = w.WsGemm(M, M, tile[2], tile, P, np_, nc, "bf16", load_path, calibration="empty", split=split)
+    epi = w.WsGemm(M, M, tile[2], tile, P, np_, nc, "bf16", load_path, calibration="epilogue", split=split)
     try:
         st = torch.cuda.current_stream().cuda_stream
         a, b, c = A.data_ptr(), B.data_ptr(), C.data_ptr()
@@ -102,13 +104,13 @@ def fixed_costs_us(M, tile, np_, load_path, A, B, C, warmup):
         epi.close()
 
 
-def per_iteration_us(kind, tile, np_, load_path, bufs, steps, warmup):
+def per_iteration_us(kind, tile, np_, load_path, bufs, steps, warmup, nc=4, split=0, stages=None):
     """Time one workgroup spends per K-iteration, from two values of K."""
     A, B, C = bufs
     mn = C.shape[0]
     tk = tile[2]
-    t1, W = kernel_us(kind, mn, mn, K_PAIR[0], tile, np_, load_path, A, B, C, steps, warmup)
-    t2, _ = kernel_us(kind, mn, mn, K_PAIR[1], tile, np_, load_path, A, B, C, steps, warmup)
+    t1, W = kernel_us(kind, mn, mn, K_PAIR[0], tile, np_, load_path, A, B, C, steps, warmup, nc, split, stages)
+    t2, _ = kernel_us(kind, mn, mn, K_PAIR[1], tile, np_, load_path, A, B, C, steps, warmup, nc, split, stages)
     iters = W * (K_PAIR[1] - K_PAIR[0]) // tk
     return (t2 - t1) / iters, {"t_k1_us": t1, "t_k2_us": t2, "rounds": W}
 

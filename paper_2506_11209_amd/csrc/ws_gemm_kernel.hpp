@@ -1308,7 +1308,7 @@ __device__ __forceinline__ void consumer_roll(const KernelArgs& args, WSG_LDS ch
       for (int nb = 0; nb < BN; ++nb) acc[mb][nb] = f32x16_t{};
     if (!wait_counter(&full[slot], ftarget, abort_flag, args.spin_limit, args.err)) return;
     const uint32_t q0 = (uint32_t)t * S;  // the tile's first K-iteration in this workgroup's sequence
-    if (t == 0) record(q0, 4, cycles32());
+    if (tracing) record(q0, 4, cycles32());  // the tile's first slot seen full
     const uint32_t base = ring + slot * (uint32_t)G::STAGE;
     uint32_t st;
     if (tracing)
@@ -1326,7 +1326,7 @@ __device__ __forceinline__ void consumer_roll(const KernelArgs& args, WSG_LDS ch
     // never taken: M > 0) without writing C.
     if (MODE != kModeMath || args.M < 0)
       store_tile<TM, TN, G::WM, G::WN, BM, BN, GENERAL, 1>(args, acc, ti, tj, wm, wn, lane);
-    record(q0 + S - 1, 7, cycles32());
+    if (tracing) record(q0 + S - 1, 7, cycles32());
     v += Gd;
     tile_coords(v, args.tiles_m, args.tiles_n, args.group_m, &ti, &tj);
   }

@@ -2,6 +2,7 @@
 
     python -m paper_2506_11209_amd.profsummary trace  DB [--kernel SUBSTR] [--skip N]
     python -m paper_2506_11209_amd.profsummary counters DB [--kernel SUBSTR] [--group G --points JSONL]
+    python -m paper_2506_11209_amd.profsummary sweeptable SWEEP_JSONL COUNTERS_JSONL... [--scales F,W]
     python -m paper_2506_11209_amd.profsummary traffic FETCH_DB WRITE_DB CAL_FETCH_DB CAL_WRITE_DB \
         --kernel SUBSTR --point KEY [--workload NAME] [--dtype bf16] [--copy-mib 1024]
 
@@ -109,9 +110,62 @@ def traffic(fetch_db, write_db, cal_fetch_db, cal_write_db, kernel, point, copy_
     print(json.dumps(rec, indent=1))
 
 
+def sweep_table(timing_jsonl: str, counter_jsonls: list, fetch_scale: float, write_scale: float,
+                cus: int = 256, xcds: int = 8, load_path: str = "registers") -> str:
+    """Markdown table: one row per launch point of a sweep, joining the
+    timing run (sweep.py JSON lines) with the per-point counter runs
+    (`counters --group --points` output) of the same points.
+      MFMA busy  SQ_VALU_MFMA_BUSY_CYCLES per SIMD / GRBM_GUI_ACTIVE per XCD
+      LDS busy   SQ_LDS_IDX_ACTIVE per CU / GRBM_GUI_ACTIVE per XCD
+      LDS wait   SQ_WAIT_INST_LDS / SQ_WAVE_CYCLES (wave cycles waiting to
+                 issue an LDS instruction)
+      L2 hit     TCC_HIT / (TCC_HIT + TCC_MISS)
+      fetch, write  FETCH_SIZE, WRITE_SIZE scaled by a known-size copy's
+                 bytes per counted KiB: L2-to-fabric request bytes (memory
+                 side, including Infinity Cache hits), in GB per launch."""
+    import json
+    timing = {}
+    with open(timing_jsonl) as f:
+        for r in map(json.loads, f):
+            timing[r["point"]] = r
+    counters = collections.defaultdict(dict)
+    for path in counter_jsonls:
+        with open(path) as f:
+            for r in map(json.loads, f):
+                counters[r["point"]].update(r["counters"])
+    simds = 4 * cus
+    lines = ["| point | TFLOP/s | clock MHz | MFMA busy | LDS busy | LDS wait | bank conflicts | L2 hit | "
+             "fetch GB | write GB |", "|---|---|---|---|---|---|---|---|---|---|"]
+    for key, r in timing.items():
+        if not key.endswith("/" + load_path):
+            continue
+        c = counters.get(key, {})
+        if r.get("status") != "ok":
+            lines.append("| %s | %s | | | | | | | | |" % (key, r.get("status")))
+            continue
+        grbm = c.get("GRBM_GUI_ACTIVE")
+        per_xcd = grbm / xcds if grbm else None
+
+        def frac(num, den):
+            return "%.1f %%" % (100.0 * num / den) if num is not None and den else "-"
+        mfma = c.get("SQ_VALU_MFMA_BUSY_CYCLES")
+        lds = c.get("SQ_LDS_IDX_ACTIVE")
+        hit, miss = c.get("TCC_HIT"), c.get("TCC_MISS")
+        lines.append("| %s | %.0f | %s | %s | %s | %s | %s | %s | %s | %s |" % (
+            key, r["tflops"], "%.0f" % r["clock_mhz"] if r.get("clock_mhz") else "-",
+            frac(mfma / simds if mfma is not None else None, per_xcd),
+            frac(lds / cus if lds is not None else None, per_xcd),
+            frac(c.get("SQ_WAIT_INST_LDS"), c.get("SQ_WAVE_CYCLES")),
+            "%.0f" % c["SQ_LDS_BANK_CONFLICT"] if "SQ_LDS_BANK_CONFLICT" in c else "-",
+            frac(hit, (hit + miss) if hit is not None and miss is not None else None),
+            "%.2f" % (c["FETCH_SIZE"] * fetch_scale / 1e9) if "FETCH_SIZE" in c else "-",
+            "%.2f" % (c["WRITE_SIZE"] * write_scale / 1e9) if "WRITE_SIZE" in c else "-"))
+    return "\n".join(lines)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
-    ap.add_argument("mode", choices=("trace", "counters", "traffic"))
+    ap.add_argument("mode", choices=("trace", "counters", "traffic", "sweeptable"))
     ap.add_argument("db", nargs="+")
     ap.add_argument("--kernel", default=None)
     ap.add_argument("--point", default=None)
@@ -122,7 +176,13 @@ def main(argv=None):
     ap.add_argument("--group", type=int, default=0, help="trace / counters: dispatches per consecutive run")
     ap.add_argument("--points", default=None,
                     help="counters --group: the sweep's JSON lines, to label each run with its launch point")
+    ap.add_argument("--scales", default="2047.9,1024.0",
+                    help="sweeptable: FETCH_SIZE and WRITE_SIZE bytes per counted KiB (from a copy run)")
     a = ap.parse_args(argv)
+    if a.mode == "sweeptable":
+        fs, ws = (float(x) for x in a.scales.split(","))
+        print(sweep_table(a.db[0], a.db[1:], fs, ws))
+        return
     if a.mode == "traffic":
         traffic(*a.db[:4], a.kernel, a.point, a.copy_mib, a.workload, a.dtype)
         return
