@@ -173,6 +173,9 @@ def main(argv=None):
     ap.add_argument("--workload", default=None, help="traffic: workload the counters ran (default: the bench's)")
     ap.add_argument("--dtype", default="bf16", help="traffic: operand dtype of the kernel")
     ap.add_argument("--skip", type=int, default=0, help="trace: leading dispatches per kernel (or run) to drop")
+    ap.add_argument("--last", type=int, default=0,
+                    help="trace: keep only the last N dispatches per kernel (a program's timed launches after "
+                         "a warm-up of varying length)")
     ap.add_argument("--group", type=int, default=0, help="trace / counters: dispatches per consecutive run")
     ap.add_argument("--points", default=None,
                     help="counters --group: the sweep's JSON lines, to label each run with its launch point")
@@ -193,7 +196,10 @@ def main(argv=None):
                 print("run %-3d %-64s n=%-4d mean_us=%.2f median_us=%.2f min_us=%.2f" % (
                     i, name[:64], len(d), statistics.fmean(d), statistics.median(d), min(d)))
     elif a.mode == "trace":
-        for name, d in sorted(kernel_durations(a.db, a.kernel, a.skip).items(), key=lambda x: -sum(x[1])):
+        durs = kernel_durations(a.db, a.kernel, a.skip)
+        if a.last > 0:
+            durs = {k: v[-a.last:] for k, v in durs.items()}
+        for name, d in sorted(durs.items(), key=lambda x: -sum(x[1])):
             print("%-72s calls=%-5d mean_us=%.2f median_us=%.2f min_us=%.2f" % (
                 name[:72], len(d), statistics.fmean(d), statistics.median(d), min(d)))
     elif a.group > 0:
