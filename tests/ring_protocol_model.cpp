@@ -21,10 +21,22 @@
 // out; 3 bad arguments.  ThreadSanitizer reports races on the slot data
 // (and exits with its own status) when the ordering is wrong.
 //
+// With a sixth argument LAG the model follows the LDS-DMA producer and the
+// kernels' consumers more closely: a producer signals K-iteration q only
+// once it has written q + LAG (its loads stay in flight until then), and
+// before it blocks on the slot of q - P (to write q) it signals every
+// pending K-iteration, as the kernel does; a consumer checks that
+// K-iteration q + 1 is full before it releases q.  The least a blocked
+// producer may signal is every pending K-iteration up to q - P + 1 (the
+// consumers need it to release q - P); PLANT_SHORT_DRAIN stops one short of
+// that.
+//
 // Planted mistakes, selected with -D for the tests that must catch them:
 //   PLANT_EARLY_RELEASE  consumers release the slot before reading it
 //   PLANT_EARLY_READ     consumers wait for one producer signal too few
 //   PLANT_DROP_SIGNAL    producer 0 skips its signal of K-iteration T/2
+//   PLANT_SHORT_DRAIN    (with LAG) a blocked producer signals pending
+//                        K-iterations only up to q - P
 #include <atomic>
 #include <chrono>
 #include <cstdint>
@@ -41,6 +53,7 @@ constexpr int kChunks = 8;  // words each producer writes per slot use
 
 struct Ring {
   uint32_t P, NP, NC, T;
+  int lag = -1;  // < 0: signal each K-iteration as soon as it is written
   long long limit_ms;
   std::vector<std::atomic<uint32_t>> full, empty;
   std::vector<uint64_t> data;  // [P][NP][kChunks], plain memory
@@ -95,6 +108,35 @@ void producer(Ring& r, uint32_t p) {
   }
 }
 
+// Producer with deferred signals (LAG >= 0); the drain before a blocking
+// wait keeps the consumers' one-K-iteration look-ahead satisfied.
+void producer_deferred(Ring& r, uint32_t p) {
+  const uint32_t lag = (uint32_t)r.lag;
+  uint32_t q_sig = 0;
+  auto publish = [&]() {
+    r.full[wsg::ring_slot(q_sig, r.P)].fetch_add(1, std::memory_order_release);
+    ++q_sig;
+  };
+  for (uint32_t q = 0; q < r.T; ++q) {
+    const uint32_t slot = wsg::ring_slot(q, r.P);
+    if (wsg::ring_use(q, r.P) > 0) {
+      const uint32_t need = wsg::ring_empty_target(q, r.P, r.NC);
+      if ((int32_t)(r.empty[slot].load(std::memory_order_acquire) - need) < 0) {
+#ifdef PLANT_SHORT_DRAIN
+        while (q_sig + r.P <= q) publish();
+#else
+        while (q_sig < q) publish();
+#endif
+        if (!wait_for(r, r.empty[slot], need)) return;
+      }
+    }
+    uint64_t* d = r.share(slot, p);
+    for (int c = 0; c < kChunks; ++c) d[c] = tag(q, p, c);
+    if (q + 1 - q_sig > lag) publish();
+  }
+  while (q_sig < r.T) publish();
+}
+
 void consume(Ring& r, uint32_t q, uint32_t slot, uint32_t target) {
 #ifdef PLANT_EARLY_READ
   target -= 1;
@@ -108,6 +150,10 @@ void consume(Ring& r, uint32_t q, uint32_t slot, uint32_t target) {
     for (int c = 0; c < kChunks; ++c)
       if (d[c] != tag(q, p, c)) r.mismatches.fetch_add(1);
   }
+  // the kernels' consumers see K-iteration q + 1 full before releasing q
+  if (r.lag >= 0 && q + 1 < r.T &&
+      !wait_for(r, r.full[wsg::ring_slot(q + 1, r.P)], wsg::ring_full_target(q + 1, r.P, r.NP)))
+    return;
 #ifndef PLANT_EARLY_RELEASE
   r.empty[slot].fetch_add(1, std::memory_order_release);
 #endif
@@ -133,22 +179,26 @@ void consumer_incremental(Ring& r) {
 }  // namespace
 
 int main(int argc, char** argv) {
-  if (argc != 6) {
-    std::fprintf(stderr, "usage: %s P NP NC T WAIT_LIMIT_MS\n", argv[0]);
+  if (argc != 6 && argc != 7) {
+    std::fprintf(stderr, "usage: %s P NP NC T WAIT_LIMIT_MS [LAG]\n", argv[0]);
     return 3;
   }
   const long P = std::atol(argv[1]), NP = std::atol(argv[2]), NC = std::atol(argv[3]);
   const long T = std::atol(argv[4]);
   const long long limit = std::atoll(argv[5]);
   if (P < 1 || P > 64 || NP < 1 || NP > 64 || NC < 1 || NC > 64 || T < 1 || limit < 1) return 3;
+  const long lag = argc == 7 ? std::atol(argv[6]) : -1;
+  // a consumer that looks one K-iteration ahead needs two slots at least
+  if (lag < -1 || lag > 64 || (lag >= 0 && P < 2)) return 3;
   Ring r((uint32_t)P, (uint32_t)NP, (uint32_t)NC, (uint32_t)T, limit);
+  r.lag = (int)lag;
   std::vector<std::thread> th;
-  for (uint32_t p = 0; p < r.NP; ++p) th.emplace_back(producer, std::ref(r), p);
+  for (uint32_t p = 0; p < r.NP; ++p) th.emplace_back(lag >= 0 ? producer_deferred : producer, std::ref(r), p);
   for (uint32_t c = 0; c < r.NC; ++c)
     th.emplace_back((c % 2) ? consumer_incremental : consumer_closed_form, std::ref(r));
   for (auto& t : th) t.join();
-  std::printf("P=%ld NP=%ld NC=%ld T=%ld timeouts=%d mismatches=%d\n", P, NP, NC, T, r.timeouts.load(),
-              r.mismatches.load());
+  std::printf("P=%ld NP=%ld NC=%ld T=%ld lag=%ld timeouts=%d mismatches=%d\n", P, NP, NC, T, lag,
+              r.timeouts.load(), r.mismatches.load());
   if (r.timeouts.load()) return 2;
   if (r.mismatches.load()) return 1;
   return 0;
