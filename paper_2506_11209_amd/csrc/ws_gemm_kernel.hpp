@@ -19,7 +19,7 @@
 //    output block 2 x 2.
 //  * Producers move a tile in 16-byte chunks, 1 KiB per wave instruction,
 //    either staged through VGPRs several K-iterations ahead
-//    (global_load_dwordx4, then ds_write_b128 once the slot is free; the
+//    (buffer_load_dwordx4, then ds_write_b128 once the slot is free; the
 //    default) or with global_load_lds_dwordx4 straight into the slot.  The
 //    LDS placement of every chunk is fixed by the lane; the layout below is
 //    produced by choosing which global chunk each lane fetches.
@@ -725,7 +725,7 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
 
 // ---------------------------------------------------------------------------
 // Register-staged producer (DMA warp).  The wave loads its share of the tiles
-// of K-iteration q + L into VGPRs (global_load_dwordx4) while K-iteration q
+// of K-iteration q + L into VGPRs (buffer_load_dwordx4) while K-iteration q
 // waits in registers for its slot; once the slot is free it writes q with
 // ds_write_b128 and signals.  Bytes in flight per wave are L iterations'
 // worth, independent of the LDS ring depth: producer waves get the kernel's
@@ -733,6 +733,21 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
 // it idle.  The LDS layout is the one the LDS-DMA producer writes.
 // ---------------------------------------------------------------------------
 typedef __attribute__((ext_vector_type(4))) int i32x4_t;
+
+// Loads of the register-staged producer go through a raw buffer resource
+// over the K-iteration's tile panel: the base sits in SGPRs and each lane
+// adds a 32-bit byte offset (panel offsets stay below 2^31, checked by the
+// plan), so a load needs no 64-bit address arithmetic on the vector ALU of a
+// SIMD whose other waves issue MFMAs.  Word 3 of the descriptor: data format
+// 32 bits (field at bits 15-18 = 4), every other field zero (no swizzle, no
+// index stride); the record count is the largest, so no offset is clipped.
+constexpr int kRawBufferWord3 = 0x00020000;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, -1, kRawBufferWord3);
+}
+__device__ __forceinline__ i32x4_t panel_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(i32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 0));
+}
 
 template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B,
           bool GENERAL>
@@ -826,6 +841,7 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
       interior = rows_left >= TM && cols_left >= TN && k_left >= TK;
       edge = (edge & ~(1u << u)) | ((interior ? 0u : 1u) << u);
     }
+    const __amdgpu_buffer_rsrc_t ra = panel_rsrc(a_src), rb = panel_rsrc(b_src);
     if (GENERAL && !interior) {
       // K and N are multiples of 8, so a 16-byte chunk is wholly inside or
       // wholly outside; the tile origin is always inside.
@@ -837,7 +853,7 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
         const int kc = 8 * ((q % G::CA) ^ swz_a<TK>(r));
         const bool ok = r < rows_left && kc < k_left;
         m |= (uint32_t)ok << n;
-        stage[u][n] = *(const i32x4_t*)(a_src + (ok ? goff[n] : 0u));
+        stage[u][n] = panel_load16(ra, ok ? goff[n] : 0u);
       }
 #pragma unroll
       for (int n = 0; n < B_PER; ++n) {
@@ -847,15 +863,14 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
         const int nc8 = (blk % G::NQ) * 16 + (w & 1) * 8;
         const bool ok = kr < k_left && nc8 < cols_left;
         m |= (uint32_t)ok << (A_PER + n);
-        stage[u][A_PER + n] = *(const i32x4_t*)(b_src + (ok ? goff[A_PER + n] : 0u));
+        stage[u][A_PER + n] = panel_load16(rb, ok ? goff[A_PER + n] : 0u);
       }
       vmask[u] = m;
     } else {
 #pragma unroll
-      for (int n = 0; n < A_PER; ++n) stage[u][n] = *(const i32x4_t*)(a_src + goff[n]);
+      for (int n = 0; n < A_PER; ++n) stage[u][n] = panel_load16(ra, goff[n]);
 #pragma unroll
-      for (int n = 0; n < B_PER; ++n)
-        stage[u][A_PER + n] = *(const i32x4_t*)(b_src + goff[A_PER + n]);
+      for (int n = 0; n < B_PER; ++n) stage[u][A_PER + n] = panel_load16(rb, goff[A_PER + n]);
     }
     if (q_iss + 1 < total) {
       ++q_iss;
