@@ -85,7 +85,8 @@ typedef enum {
 typedef enum {
   WS_LOAD_REGISTERS = 0, /* buffer_load_dwordx4 into VGPRs several K-iterations ahead, then
                             ds_write_b128 once the slot is free (more bytes in flight) */
-  WS_LOAD_DMA = 1        /* global_load_lds_dwordx4 straight into the slot once it is free */
+  WS_LOAD_DMA = 1        /* buffer_load_dwordx4 with the lds bit, straight into the slot once it
+                            is free */
 } ws_load_path;
 
 typedef struct {

@@ -20,7 +20,7 @@
 //  * Producers move a tile in 16-byte chunks, 1 KiB per wave instruction,
 //    either staged through VGPRs several K-iterations ahead
 //    (buffer_load_dwordx4, then ds_write_b128 once the slot is free; the
-//    default) or with global_load_lds_dwordx4 straight into the slot.  The
+//    default) or with buffer_load_dwordx4 ... lds straight into the slot.  The
 //    LDS placement of every chunk is fixed by the lane; the layout below is
 //    produced by choosing which global chunk each lane fetches.
 //  * 1:1 split (NP == NC): every producer loads a share of the A tile and then
@@ -575,6 +575,27 @@ __device__ __forceinline__ int first_slot(const KernelArgs& args) {
   return args.xcd_remap ? xcd_slot(blockIdx.x, G) : (int)blockIdx.x;
 }
 
+typedef __attribute__((ext_vector_type(4))) int i32x4_t;
+
+// Producer loads go through a raw buffer resource over the K-iteration's
+// tile panel: the base sits in SGPRs and each lane adds a 32-bit byte offset
+// (panel offsets stay below 2^31, checked by the plan), so a load needs no
+// 64-bit address arithmetic on the vector ALU of a SIMD whose other waves
+// issue MFMAs.  Word 3 of the descriptor: data format
+// 32 bits (field at bits 15-18 = 4), every other field zero (no swizzle, no
+// index stride); the record count is the largest, so no offset is clipped.
+constexpr int kRawBufferWord3 = 0x00020000;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, -1, kRawBufferWord3);
+}
+__device__ __forceinline__ i32x4_t panel_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(i32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 0));
+}
+// 16 bytes per lane straight into LDS: lane l's bytes land at dst + 16 l.
+__device__ __forceinline__ void panel_load16_lds(__amdgpu_buffer_rsrc_t r, WSG_LDS void* dst, uint32_t byte_off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, byte_off, 0, 0, 0);
+}
+
 // ---------------------------------------------------------------------------
 // Producer (DMA warp).  Waits for a free slot, streams its share of the A
 // and/or B tile of one K-iteration into that slot, and signals the slot full
@@ -692,21 +713,17 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
       WSG_LDS char* a_dst = smem + kHeaderBytes + slot * G::STAGE;
       WSG_LDS char* b_dst = a_dst + G::A_BYTES;
       if constexpr (DO_A) {
-        const char* src = (const char*)(a_tile + kk * TK);
+        const __amdgpu_buffer_rsrc_t src = panel_rsrc(a_tile + kk * TK);
 #pragma unroll
         for (int n = 0; n < A_PER; ++n)
-          __builtin_amdgcn_global_load_lds((const void*)(src + a_goff[n]),
-                                           (WSG_LDS void*)(a_dst + (a_rank + n * A_GROUP) * 1024),
-                                           16, 0, 0);
+          panel_load16_lds(src, (WSG_LDS void*)(a_dst + (a_rank + n * A_GROUP) * 1024), a_goff[n]);
       }
       if constexpr (DO_B) {
         if (tracing && b_rank == 0) stamp(q, 1, &full[kStampIssueB + slot], cycles32());
-        const char* src = (const char*)(b_tile + (int64_t)kk * TK * N);
+        const __amdgpu_buffer_rsrc_t src = panel_rsrc(b_tile + (int64_t)kk * TK * N);
 #pragma unroll
         for (int n = 0; n < B_PER; ++n)
-          __builtin_amdgcn_global_load_lds((const void*)(src + b_goff[n]),
-                                           (WSG_LDS void*)(b_dst + (b_rank + n * B_GROUP) * 1024),
-                                           16, 0, 0);
+          panel_load16_lds(src, (WSG_LDS void*)(b_dst + (b_rank + n * B_GROUP) * 1024), b_goff[n]);
       }
       // signal(): iteration q - lag has landed once at most `lag` newer ones are in flight.
       if (q + 1 - q_sig > lag) {
@@ -732,23 +749,6 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
 // full VGPR allocation (sized for the consumers) and would otherwise leave
 // it idle.  The LDS layout is the one the LDS-DMA producer writes.
 // ---------------------------------------------------------------------------
-typedef __attribute__((ext_vector_type(4))) int i32x4_t;
-
-// Loads of the register-staged producer go through a raw buffer resource
-// over the K-iteration's tile panel: the base sits in SGPRs and each lane
-// adds a 32-bit byte offset (panel offsets stay below 2^31, checked by the
-// plan), so a load needs no 64-bit address arithmetic on the vector ALU of a
-// SIMD whose other waves issue MFMAs.  Word 3 of the descriptor: data format
-// 32 bits (field at bits 15-18 = 4), every other field zero (no swizzle, no
-// index stride); the record count is the largest, so no offset is clipped.
-constexpr int kRawBufferWord3 = 0x00020000;
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc(const void* base) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, -1, kRawBufferWord3);
-}
-__device__ __forceinline__ i32x4_t panel_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
-  return __builtin_bit_cast(i32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 0));
-}
-
 template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B,
           bool GENERAL>
 __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LDS char* smem,

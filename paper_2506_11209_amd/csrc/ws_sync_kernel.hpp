@@ -8,7 +8,8 @@
 //
 // Same tiling, LDS layout, operand reads, MFMA and epilogue as the
 // warp-specialised kernel (ws_gemm_kernel.hpp), so the two differ only in the
-// organisation of the work.  Loads use global_load_lds_dwordx4.
+// organisation of the work.  Loads go straight into LDS (buffer_load_dwordx4
+// with the lds bit, through the same tile-panel buffer resources).
 #pragma once
 
 #include "ws_gemm_kernel.hpp"
@@ -62,18 +63,15 @@ __global__ void __launch_bounds__(NC * 64) ws_sync_kernel(KernelArgs args) {
     b_goff[n] = (uint32_t)((kq * 4 + (w >> 1)) * N + nq * 16 + (w & 1) * 8) * 2u;
   }
   auto issue = [&](int ti, int tj, int kk, int slot) {
-    const char* a_src = (const char*)(args.A + (int64_t)ti * TM * K + kk * TK);
-    const char* b_src = (const char*)(args.B + (int64_t)kk * TK * N + (int64_t)tj * TN);
+    const __amdgpu_buffer_rsrc_t a_src = panel_rsrc(args.A + (int64_t)ti * TM * K + kk * TK);
+    const __amdgpu_buffer_rsrc_t b_src = panel_rsrc(args.B + (int64_t)kk * TK * N + (int64_t)tj * TN);
     WSG_LDS char* dst = ring + slot * G::STAGE;
 #pragma unroll
     for (int n = 0; n < G::A_PER; ++n)
-      __builtin_amdgcn_global_load_lds((const void*)(a_src + a_goff[n]),
-                                       (WSG_LDS void*)(dst + (wave + n * NC) * 1024), 16, 0, 0);
+      panel_load16_lds(a_src, (WSG_LDS void*)(dst + (wave + n * NC) * 1024), a_goff[n]);
 #pragma unroll
     for (int n = 0; n < G::B_PER; ++n)
-      __builtin_amdgcn_global_load_lds((const void*)(b_src + b_goff[n]),
-                                       (WSG_LDS void*)(dst + G::A_BYTES + (wave + n * NC) * 1024), 16,
-                                       0, 0);
+      panel_load16_lds(b_src, (WSG_LDS void*)(dst + G::A_BYTES + (wave + n * NC) * 1024), b_goff[n]);
   };
 
   // Operand offsets (same layout and reads as the specialised consumers).
