@@ -595,6 +595,81 @@ __device__ __forceinline__ i32x4_t panel_load16(__amdgpu_buffer_rsrc_t r, uint32
 __device__ __forceinline__ void panel_load16_lds(__amdgpu_buffer_rsrc_t r, WSG_LDS void* dst, uint32_t byte_off) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, byte_off, 0, 0, 0);
 }
+// Events of one kind that a producer wave stores into its workgroup's trace
+// record, batched: lane k of `vals` holds the event of K-iteration base + k
+// (events arrive for consecutive K-iterations), and 64 of them go out in one
+// store.  A store sits in the same vector-memory counter as the loads the
+// wave waits for before it writes a slot, so one store per K-iteration would
+// hold every slot back behind its write acknowledgement.
+struct StampBatch {
+  uint32_t vals = 0;
+  uint32_t base = 0, n = 0;
+};
+// Adds the event of K-iteration iq; true when the batch is full.
+__device__ __forceinline__ bool stamp_put(StampBatch& b, uint32_t iq, uint32_t value, int lane) {
+  if (b.n == 0) b.base = iq;
+  b.vals = ((uint32_t)lane == b.n) ? value : b.vals;
+  return ++b.n == 64;
+}
+__device__ __forceinline__ void stamp_store(const StampBatch& b, __amdgpu_buffer_rsrc_t rec, int ev,
+                                            uint32_t limit, int lane) {
+  const uint32_t iq = b.base + (uint32_t)lane;
+  if ((uint32_t)lane < b.n && iq < limit)
+    __builtin_amdgcn_raw_buffer_store_b32(b.vals, rec, (int)((iq * kTraceEvents + (uint32_t)ev) * 4u), 0, 0);
+}
+
+// Events 0-3 of a producer wave (issue of its A / B loads of K-iteration q,
+// their landing in the slot); A and B share one clock reading each.  With
+// DIRECT (the eight-consumer arrangement, whose consumer does not copy stamps
+// out of the LDS header) they go straight into the workgroup's trace record,
+// batched; otherwise into the LDS header for consumer wave 0 to copy.
+template <bool DIRECT>
+struct ProducerStamps {
+  // Bit 0: this wave stamps the A events, bit 1: the B events.  Kept as a
+  // scalar integer, not as bools (those would be materialised as lane masks
+  // through vector instructions).
+  uint32_t who;
+  int lane;
+  uint32_t limit;
+  __amdgpu_buffer_rsrc_t rec;
+  StampBatch iss, land;
+  __device__ ProducerStamps(const KernelArgs& args, bool stamps_a, bool stamps_b, int lane_)
+      : who(__builtin_amdgcn_readfirstlane((stamps_a ? 1u : 0u) | (stamps_b ? 2u : 0u))), lane(lane_),
+        limit(DIRECT ? (uint32_t)args.trace_iters : 0u),
+        rec(panel_rsrc(DIRECT ? args.trace + (size_t)blockIdx.x * args.trace_iters * kTraceEvents : nullptr)) {}
+  __device__ void flush(StampBatch& b, int ev_a, int ev_b) {
+    if (who & 1u) stamp_store(b, rec, ev_a, limit, lane);
+    if (who & 2u) stamp_store(b, rec, ev_b, limit, lane);
+    b.n = 0;
+  }
+  __device__ void put(StampBatch& b, int ev_a, int ev_b, uint32_t q, uint32_t t, WSG_LDS uint32_t* hdr_a,
+                      WSG_LDS uint32_t* hdr_b) {
+    if constexpr (DIRECT) {
+      if (who != 0u && stamp_put(b, q, t, lane)) flush(b, ev_a, ev_b);
+    } else {
+      if (who & 1u) lds_stamp(hdr_a, t);
+      if (who & 2u) lds_stamp(hdr_b, t);
+    }
+  }
+  __device__ void issued(uint32_t q, uint32_t t, WSG_LDS uint32_t* hdr_a, WSG_LDS uint32_t* hdr_b) {
+    put(iss, 0, 1, q, t, hdr_a, hdr_b);
+  }
+  __device__ void landed(uint32_t q, uint32_t t, WSG_LDS uint32_t* hdr_a, WSG_LDS uint32_t* hdr_b) {
+    put(land, 2, 3, q, t, hdr_a, hdr_b);
+  }
+  __device__ void finish() {
+    if constexpr (DIRECT) {
+      flush(iss, 0, 1);
+      flush(land, 2, 3);
+    }
+  }
+};
+
+// A traced kernel runs its producer loop's traced instance only in the
+// workgroups that record events; the others run the plain instance.
+__device__ __forceinline__ bool traced_workgroup(const KernelArgs& args) {
+  return args.trace != nullptr && (int)blockIdx.x < args.trace_wgs;
+}
 
 // ---------------------------------------------------------------------------
 // Producer (DMA warp).  Waits for a free slot, streams its share of the A
@@ -657,26 +732,13 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
     b_goff[n] = (uint32_t)((kq * 4 + (w >> 1)) * N + nq * 16 + (w & 1) * 8) * 2u;
   }
 
-  const bool tracing = TRACE && args.trace != nullptr && (int)blockIdx.x < args.trace_wgs;
-  // The eight-consumer arrangement's consumer does not copy stamps out of the
-  // LDS header: its producers store their events straight into the record.
-  uint32_t* trec = (tracing && NC == 8) ? args.trace + (size_t)blockIdx.x * args.trace_iters * kTraceEvents
-                                        : nullptr;
-  auto stamp = [&](uint32_t iq, int ev, WSG_LDS uint32_t* hdr, uint32_t value) {
-    if (trec) {
-      if (iq < (uint32_t)args.trace_iters && lane == 0) trec[iq * kTraceEvents + ev] = value;
-    } else {
-      lds_stamp(hdr, value);
-    }
-  };
+  // TRACE: this instance runs only in workgroups that record events.
+  constexpr bool tracing = TRACE;
+  ProducerStamps<TRACE && NC == 8> stamps(args, DO_A && a_rank == 0, DO_B && b_rank == 0, lane);
   // signal(): data of the slot has landed; stamp its landing time first when tracing.
   auto publish = [&](uint32_t pq) {
     const uint32_t pslot = ring_slot(pq, (uint32_t)args.stages);
-    if (tracing) {
-      const uint32_t t = cycles32();
-      if (DO_A && a_rank == 0) stamp(pq, 2, &full[kStampLandA + pslot], t);
-      if (DO_B && b_rank == 0) stamp(pq, 3, &full[kStampLandB + pslot], t);
-    }
+    if constexpr (tracing) stamps.landed(pq, cycles32(), &full[kStampLandA + pslot], &full[kStampLandB + pslot]);
     lds_signal(&full[pslot]);
   };
   const int Gd = gridDim.x;
@@ -709,7 +771,7 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
       }
       debug_delay(args.producer_delay);
       compiler_fence();
-      if (tracing && a_rank == 0 && DO_A) stamp(q, 0, &full[kStampIssueA + slot], cycles32());
+      if constexpr (tracing) stamps.issued(q, cycles32(), &full[kStampIssueA + slot], &full[kStampIssueB + slot]);
       WSG_LDS char* a_dst = smem + kHeaderBytes + slot * G::STAGE;
       WSG_LDS char* b_dst = a_dst + G::A_BYTES;
       if constexpr (DO_A) {
@@ -719,7 +781,6 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
           panel_load16_lds(src, (WSG_LDS void*)(a_dst + (a_rank + n * A_GROUP) * 1024), a_goff[n]);
       }
       if constexpr (DO_B) {
-        if (tracing && b_rank == 0) stamp(q, 1, &full[kStampIssueB + slot], cycles32());
         const __amdgpu_buffer_rsrc_t src = panel_rsrc(b_tile + (int64_t)kk * TK * N);
 #pragma unroll
         for (int n = 0; n < B_PER; ++n)
@@ -738,6 +799,7 @@ __device__ __forceinline__ void producer_loop(const KernelArgs& args, WSG_LDS ch
     publish(q_sig);
     ++q_sig;
   }
+  stamps.finish();
 }
 
 // ---------------------------------------------------------------------------
@@ -789,18 +851,9 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
   }
   const uint32_t lane16 = (uint32_t)lane * 16u;
 
-  const bool tracing = TRACE && args.trace != nullptr && (int)blockIdx.x < args.trace_wgs;
-  // The eight-consumer arrangement's consumer does not copy stamps out of the
-  // LDS header: its producers store their events straight into the record.
-  uint32_t* trec = (tracing && NC == 8) ? args.trace + (size_t)blockIdx.x * args.trace_iters * kTraceEvents
-                                        : nullptr;
-  auto stamp = [&](uint32_t iq, int ev, WSG_LDS uint32_t* hdr, uint32_t value) {
-    if (trec) {
-      if (iq < (uint32_t)args.trace_iters && lane == 0) trec[iq * kTraceEvents + ev] = value;
-    } else {
-      lds_stamp(hdr, value);
-    }
-  };
+  // TRACE: this instance runs only in workgroups that record events.
+  constexpr bool tracing = TRACE;
+  ProducerStamps<TRACE && NC == 8> stamps(args, DO_A && a_rank == 0, DO_B && b_rank == 0, lane);
   const int Gd = gridDim.x;
   const int g0 = first_slot(args);
   const int my_tiles = (args.num_tiles - g0 + Gd - 1) / Gd;
@@ -814,7 +867,10 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
   tile_coords(v_i, args.tiles_m, args.tiles_n, args.group_m, &ti_i, &tj_i);
 
   i32x4_t stage[L][LOADS];
-  uint32_t t_issue[L];
+  // Traced: one clock reading per K-iteration, taken once K-iteration q is in
+  // its slot, stands for the landing of q and the issue of q + L (the loads
+  // go out right after q's signal).
+  uint32_t t_issue[L], t_now = 0;
   // GENERAL: bit n of vmask[u] says chunk n of staged iteration u lies inside
   // A / B.  A chunk outside is fetched from the tile's first element (always
   // inside) and written to LDS as zeros, so partial tiles and the tail of the
@@ -826,7 +882,7 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
   // loop has the same number of loads in flight and the compiler's vmcnt
   // waits before each ds_write allow exactly L - 1 newer iterations.
   auto issue = [&](int u) {
-    if (tracing) t_issue[u] = cycles32();
+    if constexpr (tracing) t_issue[u] = t_now;
     const char* a_src = (const char*)(args.A + (int64_t)ti_i * TM * K + kk_i * TK);
     const char* b_src = (const char*)(args.B + (int64_t)kk_i * TK * N + (int64_t)tj_i * TN);
     // GENERAL: a K-iteration whose tiles lie wholly inside A and B (the
@@ -882,6 +938,7 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
     }
   };
 
+  if constexpr (tracing) t_now = cycles32();
 #pragma unroll
   for (int u = 0; u < L; ++u) issue(u);
 
@@ -914,22 +971,17 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
 #pragma unroll
       for (int n = 0; n < B_PER; ++n)
         *(WSG_LDS i32x4_t*)(base + G::A_BYTES + (b_rank + n * B_GROUP) * 1024) = stage[u][A_PER + n];
-      if (tracing) {
-        const uint32_t t = cycles32();
-        if (DO_A && a_rank == 0) {
-          stamp(q, 0, &full[kStampIssueA + slot], t_issue[u]);
-          stamp(q, 2, &full[kStampLandA + slot], t);
-        }
-        if (DO_B && b_rank == 0) {
-          stamp(q, 1, &full[kStampIssueB + slot], t_issue[u]);
-          stamp(q, 3, &full[kStampLandB + slot], t);
-        }
+      if constexpr (tracing) {
+        t_now = cycles32();
+        stamps.issued(q, t_issue[u], &full[kStampIssueA + slot], &full[kStampIssueB + slot]);
+        stamps.landed(q, t_now, &full[kStampLandA + slot], &full[kStampLandB + slot]);
       }
       lds_signal(&full[slot]);  // waits for the LDS writes, then signals
       }
       issue(u);  // refill this register stage with K-iteration q + L
     }
   }
+  stamps.finish();
   wait_vmcnt<0>();
 }
 
@@ -955,20 +1007,33 @@ __device__ __forceinline__ void producer_signal_only(const KernelArgs& args, WSG
   }
 }
 
+// One producer wave's loop on the configured load path; STAMP: it records
+// trace events.
+template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, bool STAMP, bool DO_A, bool DO_B,
+          bool GENERAL>
+__device__ __forceinline__ void producer_run(const KernelArgs& args, WSG_LDS char* smem, int a_rank, int b_rank,
+                                             int lane) {
+  if constexpr (GENERAL) {  // partial tiles possible: always register-staged
+    producer_loop_reg<TM, TN, TK, NC, NPW, SPLIT, BF16, STAMP, DO_A, DO_B, true>(args, smem, a_rank, b_rank,
+                                                                            lane);
+  } else if (args.load_path == 1) {  // wave-uniform: 0 = register-staged, 1 = LDS-DMA
+    producer_loop<TM, TN, TK, NC, NPW, SPLIT, BF16, STAMP, DO_A, DO_B>(args, smem, a_rank, b_rank, lane);
+  } else {
+    producer_loop_reg<TM, TN, TK, NC, NPW, SPLIT, BF16, STAMP, DO_A, DO_B, false>(args, smem, a_rank, b_rank,
+                                                                             lane);
+  }
+}
+
 template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, bool TRACE, bool DO_A, bool DO_B,
           bool GENERAL>
 __device__ __forceinline__ void producer_share(const KernelArgs& args, WSG_LDS char* smem, int a_rank,
                                                int b_rank, int lane) {
   if constexpr (!DO_A && !DO_B) {
     producer_signal_only<NC>(args, smem);
-  } else if constexpr (GENERAL) {  // partial tiles possible: always register-staged
-    producer_loop_reg<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, DO_A, DO_B, true>(args, smem, a_rank, b_rank,
-                                                                            lane);
-  } else if (args.load_path == 1) {  // wave-uniform: 0 = register-staged, 1 = LDS-DMA
-    producer_loop<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, DO_A, DO_B>(args, smem, a_rank, b_rank, lane);
+  } else if (TRACE && traced_workgroup(args)) {
+    producer_run<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, DO_A, DO_B, GENERAL>(args, smem, a_rank, b_rank, lane);
   } else {
-    producer_loop_reg<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, DO_A, DO_B, false>(args, smem, a_rank, b_rank,
-                                                                             lane);
+    producer_run<TM, TN, TK, NC, NPW, SPLIT, BF16, false, DO_A, DO_B, GENERAL>(args, smem, a_rank, b_rank, lane);
   }
 }
 

@@ -78,9 +78,17 @@ def _bytes_at(elf: bytes, secs, value: int, size: int) -> bytes:
     raise ValueError("symbol outside every section")
 
 
+# Bytes 16-23 of an AMDHSA kernel descriptor hold the byte offset from the
+# descriptor to the kernel's entry: it moves whenever another kernel of the
+# code object changes size, so the fingerprint leaves it out.
+_KD_ENTRY_OFFSET = slice(16, 24)
+
+
 def kernel_fingerprint(symbol: str, lib_path: str | None = None) -> str:
-    """16 hex digits of SHA-256 over the kernel's code and descriptor bytes;
-    raises LookupError if the library holds no such kernel."""
+    """16 hex digits of SHA-256 over the kernel's code and descriptor bytes
+    (without the descriptor's entry offset, which depends on where the
+    kernel sits in the code object); raises LookupError if the library holds
+    no such kernel."""
     if lib_path is None:
         lib_path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libwsgemm.so")
     with open(lib_path, "rb") as f:
@@ -92,7 +100,10 @@ def kernel_fingerprint(symbol: str, lib_path: str | None = None) -> str:
             h = hashlib.sha256()
             for name in (symbol, symbol + ".kd"):
                 value, size = syms[name]
-                h.update(name.encode() + _bytes_at(co, secs, value, size))
+                data = bytearray(_bytes_at(co, secs, value, size))
+                if name.endswith(".kd"):
+                    data[_KD_ENTRY_OFFSET] = bytes(8)
+                h.update(name.encode() + bytes(data))
             return h.hexdigest()[:16]
     raise LookupError("kernel %s not found in %s" % (symbol, lib_path))
 
