@@ -147,7 +147,10 @@ const char* ws_gemm_last_error(void);
 /* Validate a configuration and derive its launch without touching a GPU.
  * num_cus: compute units to plan for; wgs_per_cu: resident workgroups per CU
  * (<= 0 derives it from LDS use, wave count and the registers the compiled
- * kernel allocates, recorded at build time).  Fills *out on WS_OK. */
+ * kernel allocates, recorded at build time).  The grid uses u <= wgs_per_cu
+ * workgroups per CU, the u that minimises rounds x u (the largest on a tie),
+ * so that no partly filled last round runs at the shared CUs' pace.
+ * Fills *out on WS_OK. */
 ws_status ws_gemm_plan(int64_t M, int64_t N, int64_t K, const ws_gemm_config* cfg,
                        int32_t num_cus, int32_t wgs_per_cu, ws_gemm_plan_info* out);
 

@@ -165,7 +165,22 @@ inline int plan_launch(const PlanIn& in, PlanOut* out) {
     if (kMaxWgsPerCu < occ) occ = kMaxWgsPerCu;
   }
   if (occ < 1) occ = 1;
-  int64_t slots = (int64_t)in.num_cus * occ;
+  // Of the occ workgroups a CU can hold, use the count u that minimises
+  // rounds x u (workgroups sharing a CU progress about u times slower), the
+  // largest on a tie: a last round that only part of the slots take costs a
+  // whole round of the shared CUs (4096 tiles on 256 CUs: five resident
+  // workgroups would need four rounds of five, four need four rounds of four).
+  int use = 1;
+  int64_t best = -1;
+  for (int u = 1; u <= occ; ++u) {
+    const int64_t slots_u = (int64_t)in.num_cus * u;
+    const int64_t cost = ((tiles + slots_u - 1) / slots_u) * u;
+    if (best < 0 || cost <= best) {
+      best = cost;
+      use = u;
+    }
+  }
+  int64_t slots = (int64_t)in.num_cus * use;
   const int grid = (int)(tiles < slots ? tiles : slots);
   const int xcd_remap = (grid % 8 == 0) ? 1 : 0;  // the remap needs whole XCD groups
 

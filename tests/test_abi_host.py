@@ -71,6 +71,27 @@ def test_plan_every_workload_point(name):
         assert info.split == split_of(pt) and info.block == 64 * (np_ + nc)
 
 
+@pytest.mark.parametrize("tiles_m,tiles_n,resident,expect_per_cu", [
+    (64, 64, 5, 4),   # 4096 tiles: four rounds of four beat four rounds of five
+    (80, 64, 5, 5),   # 5120 tiles: four rounds of five fill every slot
+    (32, 32, 3, 2),   # 1024 tiles: 2 rounds of 2 (4) against 2 of 3 (6); 1 x 4 ties, the larger wins
+    (32, 32, 4, 4),   # 1024 tiles: one round of four
+    (1, 100, 4, 1),   # 100 tiles: fewer tiles than CUs
+])
+def test_grid_balances_rounds_against_sharing(tiles_m, tiles_n, resident, expect_per_cu):
+    # the synchronous kernel (128 x 128 x 32, ring depth 1) with the given
+    # resident workgroups per CU on 256 CUs
+    c = cfg((128, 128, 32), 1, 0, 4, "bf16")
+    s, info = w.ws_gemm_plan(128 * tiles_m, 128 * tiles_n, 64, c, 256, resident)
+    assert s == w.WS_OK
+    tiles = tiles_m * tiles_n
+    assert info.grid == min(tiles, 256 * expect_per_cu)
+    assert info.rounds == -(-tiles // info.grid)
+    # no other count of workgroups per CU costs fewer rounds x workgroups per CU
+    cost = lambda u: -(-tiles // (256 * u)) * u
+    assert all(cost(u) >= cost(expect_per_cu) for u in range(1, resident + 1))
+
+
 def test_lds_overflow_case_from_the_sweep():
     # (256,128,64) x 4 stages = 192 KiB + header > 160 KiB
     s, _ = w.ws_gemm_plan(8192, 8192, 8192, cfg((256, 128, 64), 4), 256, 1)
