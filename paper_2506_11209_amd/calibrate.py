@@ -28,8 +28,11 @@ With --table, T_MATH, T_LOAD-A, T_LOAD-B and the time of loading both tiles
 (the producers' own rate, WS_CALIB_LOAD_AB) are also measured directly for
 every tile of the accuracy grid (model_eval.py), so that the event model can
 be evaluated apart from the linear cost model; --table-tiles paper measures
-the tiles of the paper's own grid instead.  Writes one JSON document
-with every raw measurement.
+the tiles of the paper's own grid instead.  The accuracy table also holds
+the eight-consumer 256 x 256 launches (four producer waves in `split`
+groups), whose consumer the linear fits do not describe: the optimizer ranks
+them with these measured costs only.  Writes one JSON document with every
+raw measurement.
 """
 from __future__ import annotations
 
@@ -53,6 +56,8 @@ TABLE_TILES = {
                  (128, 256, 32)),
     "paper": ((64, 64, 64), (64, 128, 64), (128, 64, 64), (128, 128, 64)),
 }
+# eight consumer waves, four producer waves: (tile, stages) measured with the accuracy table
+EIGHT_CONSUMER_TILES = (((256, 256, 64), 2), ((256, 256, 32), 4))
 LDS_LIMIT = 163840
 FIXED_LAUNCHES = 200
 
@@ -115,16 +120,18 @@ def per_iteration_us(kind, tile, np_, load_path, bufs, steps, warmup, nc=4, spli
     return (t2 - t1) / iters, {"t_k1_us": t1, "t_k2_us": t2, "rounds": W}
 
 
-def costs(tile, np_, load_path, bufs, steps, warmup):
+def costs(tile, np_, load_path, bufs, steps, warmup, nc=4, split=0, stages=None):
     """Measured per-K-iteration T_LOAD-A, T_LOAD-B and T_MATH of one tile."""
-    la, ra = per_iteration_us("load_a", tile, np_, load_path, bufs, steps, warmup)
-    lb, rb = per_iteration_us("load_b", tile, np_, load_path, bufs, steps, warmup)
-    mm, rm = per_iteration_us("math", tile, np_, load_path, bufs, steps, warmup)
+    kw = dict(nc=nc, split=split, stages=stages)
+    la, ra = per_iteration_us("load_a", tile, np_, load_path, bufs, steps, warmup, **kw)
+    lb, rb = per_iteration_us("load_b", tile, np_, load_path, bufs, steps, warmup, **kw)
+    mm, rm = per_iteration_us("math", tile, np_, load_path, bufs, steps, warmup, **kw)
     return (la, ra), (lb, rb), (mm, rm)
 
 
-def calibrate(split, load_path, bufs, steps, warmup, table):
-    """table: None, or the tiles to measure one by one."""
+def calibrate(split, load_path, bufs, steps, warmup, table, eight=()):
+    """table: None, or the tiles to measure one by one; eight: (tile, stages)
+    of eight-consumer launches to add to the table."""
     np_ = 4 * split
     A, B, C = bufs
     mn = C.shape[0]
@@ -158,6 +165,14 @@ def calibrate(split, load_path, bufs, steps, warmup, table):
                          "t_load_ab": lab, "t_math": mm})
             log("table split %d %s tile %s: load A %.4f  load B %.4f  load A+B %.4f  math %.4f us" % (
                 split, load_path, tile, la, lb, lab, mm))
+        for tile, P in eight:
+            kw = dict(nc=8, split=split, stages=P)
+            (la, _), (lb, _), (mm, _) = costs(tile, 4, load_path, bufs, steps, warmup, **kw)
+            lab, _ = per_iteration_us("load_ab", tile, 4, load_path, bufs, steps, warmup, **kw)
+            rows.append({"tile": tile, "stages": P, "consumer_waves": 8, "producer_waves": 4, "t_load_a": la,
+                         "t_load_b": lb, "t_load_ab": lab, "t_math": mm})
+            log("table split %d %s tile %s, 8 + 4 waves: load A %.4f  load B %.4f  load A+B %.4f  math %.4f us"
+                % (split, load_path, tile, la, lb, lab, mm))
         rec["table"] = rows
     return rec
 
@@ -188,7 +203,9 @@ def main(argv=None):
            "calibrations": []}
     for lp in a.load_paths.split(","):
         for split in (int(x) for x in a.splits.split(",")):
-            rec = calibrate(split, lp, bufs, a.steps, a.warmup, TABLE_TILES[a.table_tiles] if a.table else None)
+            eight = EIGHT_CONSUMER_TILES if a.table and a.table_tiles == "accuracy" else ()
+            rec = calibrate(split, lp, bufs, a.steps, a.warmup, TABLE_TILES[a.table_tiles] if a.table else None,
+                            eight)
             out["calibrations"].append(rec)
             log("split %d %s: %s" % (split, lp, json.dumps(rec["params"])))
     text = json.dumps(out, indent=1)

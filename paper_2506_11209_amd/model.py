@@ -67,9 +67,16 @@ def load_calibration(path: str) -> dict:
     return out
 
 
+def table_key(split: int, load_path: str, tile, consumer_waves: int = 4):
+    """Key of a tile's measured costs in load_cost_table's result: four-consumer
+    launches by (split, load path, tile), others with the consumer count too."""
+    tile = tuple(tile)
+    return (split, load_path, tile) if consumer_waves == 4 else (split, load_path, tile, consumer_waves)
+
+
 def load_cost_table(path: str) -> dict:
-    """{(split, load_path, (tm, tn, tk)): (t_math, t_load_a, t_load_b)} from
-    a calibration file written with --table.
+    """{table_key(...): (t_math, t_load_a, t_load_b)} from a calibration file
+    written with --table.
 
     Two DMA groups load A and B concurrently, so each takes the time measured
     with only its own tile loaded.  One DMA group issues both tiles of a
@@ -87,7 +94,8 @@ def load_cost_table(path: str) -> dict:
             else:
                 la = row["t_load_ab"] * tm / (tm + tn)
                 lb = row["t_load_ab"] * tn / (tm + tn)
-            out[(rec["split"], rec["load_path"], (tm, tn, tk))] = (row["t_math"], la, lb)
+            out[table_key(rec["split"], rec["load_path"], (tm, tn, tk), row.get("consumer_waves", 4))] = (
+                row["t_math"], la, lb)
     return out
 
 
@@ -97,32 +105,35 @@ def params_dict(p: Params) -> dict:
 
 # -- configuration optimizer (Section 3.2, by exhaustive search) ---------------
 
-def compiled_configs(dtype="bf16", splits=(1, 2), consumer_waves=(4,)):
-    """(tile, producer_waves, consumer_waves) of every compiled specialised GEMM
-    kernel of the given dtype (the library is built from build.instances())."""
+def compiled_configs(dtype="bf16", splits=(1, 2), consumer_waves=(4, 8)):
+    """(tile, producer_waves, consumer_waves, split) of every compiled
+    specialised GEMM kernel of the given dtype (the library is built from
+    build.instances()) in the arrangements the calibration covers: split
+    groups of four producer waves with four consumer waves, and four producer
+    waves in one or two groups with eight consumer waves."""
     from paper_2506_11209_amd.build import MODE_GEMM, instances
     want_bf16 = 1 if dtype == "bf16" else 0
     out = set()
     for (tm, tn, tk, nc, np_, split, bf16, trace, mode, general) in instances():
-        # the arrangements the calibration covers: split groups of nc producer waves
-        if (bf16 == want_bf16 and not trace and not general and mode == MODE_GEMM and split in splits
-                and nc in consumer_waves and np_ == nc * split):
-            out.add(((tm, tn, tk), np_, nc))
+        if bf16 != want_bf16 or trace or general or mode != MODE_GEMM or split not in splits:
+            continue
+        if nc in consumer_waves and ((nc == 4 and np_ == 4 * split) or (nc == 8 and np_ == 4)):
+            out.add(((tm, tn, tk), np_, nc, split))
     return sorted(out)
 
 
 def candidates(M, N, K, dtype="bf16", splits=(1, 2), stages=range(2, 9), num_cus=256,
-               load_path="registers"):
-    """Launchable (tile, stages, producer_waves, consumer_waves, slots) for this
-    problem: compiled, ring fits in LDS, tiles divide the problem.  `slots` is
-    the planned grid (workgroups that run at once)."""
+               load_path="registers", consumer_waves=(4, 8)):
+    """Launchable (tile, stages, producer_waves, consumer_waves, slots, split)
+    for this problem: compiled, ring fits in LDS, tiles divide the problem.
+    `slots` is the planned grid (workgroups that run at once)."""
     out = []
-    for tile, np_, nc in compiled_configs(dtype, splits):
+    for tile, np_, nc, split in compiled_configs(dtype, splits, consumer_waves):
         for P in stages:
-            cfg = w.config(tile, P, np_, nc, dtype, load_path)
+            cfg = w.config(tile, P, np_, nc, dtype, load_path, split)
             s, info = w.ws_gemm_plan(M, N, K, cfg, num_cus, 0)
             if s == w.WS_OK:
-                out.append((tile, P, np_, nc, info.grid))
+                out.append((tile, P, np_, nc, info.grid, split))
     return out
 
 
@@ -132,18 +143,25 @@ def optimize(M, N, K, params_by_split: dict, cands, objective="time", persistent
     first goal) or by predicted total MATH wait (second goal; ties broken by
     time, then by the deeper ring).  params_by_split: {1: Params, 2: Params}.  With `table` (from
     load_cost_table), tiles that were measured use their own costs; the others
-    the fitted linear costs.  Returns a list of dicts, best first."""
+    the fitted linear costs.  The fits are calibrated on four-consumer kernels:
+    a candidate with another consumer count is ranked only with its own
+    measured costs, and left out without them.  A candidate is (tile, stages,
+    producer_waves, consumer_waves, slots[, split]); split defaults to
+    producer_waves / consumer_waves.  Returns a list of dicts, best first."""
     rows = []
-    for (tile, P, np_, nc, slots) in cands:
-        split = np_ // nc
-        costs = table.get((split, load_path, tuple(tile))) if table else None
+    for c in cands:
+        tile, P, np_, nc, slots = c[:5]
+        split = c[5] if len(c) > 5 else np_ // nc
+        costs = table.get(table_key(split, load_path, tile, nc)) if table else None
+        if costs is None and nc != 4:
+            continue
         if costs is not None:
             r = predict_costs(M, N, K, tile, P, slots, params_by_split[split], *costs,
                               two_dma=(split == 2), persistent=persistent)
         else:
             r = predict(M, N, K, tile, P, slots, params_by_split[split], two_dma=(split == 2),
                         persistent=persistent)
-        rows.append({"tile": tile, "stages": P, "producer_waves": np_, "consumer_waves": nc,
+        rows.append({"tile": tile, "stages": P, "producer_waves": np_, "consumer_waves": nc, "split": split,
                      "slots": slots, "time_us": r["total_us"], "wait_us": r["wait_us"],
                      "costs": "table" if costs is not None else "fit"})
     # Ties (the model gives every ring depth the same time once the pipeline

@@ -54,7 +54,7 @@ def measure(rows, M, N, K, load_path, steps, warmup):
 
     def median_us(r, nsteps, nwarm, min_seconds=0.0):
         g = w.WsGemm(M, N, K, r["tile"], r["stages"], r["producer_waves"], r["consumer_waves"], "bf16",
-                     load_path)
+                     load_path, split=r["split"])
         try:
             t0 = time.perf_counter()
             while True:
@@ -73,8 +73,8 @@ def measure(rows, M, N, K, load_path, steps, warmup):
         r["measured_pass_us"].append(median_us(r, steps, warmup))
         r["measured_us"] = min(r["measured_pass_us"])
     for r in rows:
-        print("%-14s P=%d %d:%d  predicted %9.1f us  measured %9.1f us" % (
-            "x".join(map(str, r["tile"])), r["stages"], r["producer_waves"], r["consumer_waves"],
+        print("%-14s P=%d %d:%d/%d  predicted %9.1f us  measured %9.1f us" % (
+            "x".join(map(str, r["tile"])), r["stages"], r["producer_waves"], r["consumer_waves"], r["split"],
             r["time_us"], r["measured_us"]), file=sys.stderr, flush=True)
 
 
@@ -96,8 +96,7 @@ def main(argv=None):
     M, N, K = (int(x) for x in a.mnk.split(","))
     cal = load_calibration(a.calib)
     params = {s: cal[(s, a.load_path)] for s in (1, 2) if (s, a.load_path) in cal}
-    cands = [c for c in candidates(M, N, K, num_cus=a.num_cus, load_path=a.load_path)
-             if c[2] // c[3] in params]
+    cands = [c for c in candidates(M, N, K, num_cus=a.num_cus, load_path=a.load_path) if c[5] in params]
     table = load_cost_table(a.calib) if a.costs == "table" else None
     rows = optimize(M, N, K, params, cands, a.objective, table=table, load_path=a.load_path)
     for i, r in enumerate(rows):
@@ -116,8 +115,8 @@ def main(argv=None):
             for r in rows:
                 f.write(json.dumps(r) + "\n")
     for r in rows[:a.top]:
-        print("%-14s P=%d %d:%d slots=%d predicted %9.1f us wait %9.1f us%s" % (
-            "x".join(map(str, r["tile"])), r["stages"], r["producer_waves"], r["consumer_waves"],
+        print("%-14s P=%d %d:%d/%d slots=%d predicted %9.1f us wait %9.1f us%s" % (
+            "x".join(map(str, r["tile"])), r["stages"], r["producer_waves"], r["consumer_waves"], r["split"],
             r["slots"], r["time_us"], r["wait_us"],
             ("  measured %9.1f us" % r["measured_us"]) if "measured_us" in r else ""), file=sys.stderr)
     print(json.dumps(report, default=str))

@@ -358,3 +358,32 @@ def test_optimizer_ranks_like_brute_force_with_the_oracle():
             if objective == "time":
                 assert rows[0]["time_us"] == best_time
             assert sorted(r["time_us"] for r in rows) == sorted(key(c) for c in cands)
+
+
+def test_optimizer_ranks_eight_consumer_launches_only_with_their_measured_costs(tmp_path):
+    # The linear fits describe the four-consumer kernels; an eight-consumer
+    # candidate is ranked with its own measured costs, and left out without.
+    import json
+    from paper_2506_11209_amd.model import Params, load_cost_table, optimize, table_key
+    params = {1: Params(6.5, 1.8, 3.1e6, 0.15, 1.0e5, 0.25)}
+    cal = {"calibrations": [{"split": 1, "load_path": "registers", "table": [
+        {"tile": [256, 128, 64], "stages": 3, "t_load_a": 0.5, "t_load_b": 0.3, "t_load_ab": 0.9,
+         "t_math": 1.2},
+        {"tile": [256, 256, 64], "stages": 2, "consumer_waves": 8, "producer_waves": 4, "t_load_a": 0.6,
+         "t_load_b": 0.6, "t_load_ab": 1.0, "t_math": 1.4}]}]}
+    path = tmp_path / "calib.json"
+    path.write_text(json.dumps(cal))
+    table = load_cost_table(str(path))
+    assert table[table_key(1, "registers", (256, 128, 64))] == (1.2, 0.9 * 256 / 384, 0.9 * 128 / 384)
+    assert table[table_key(1, "registers", (256, 256, 64), 8)] == (1.4, 0.5, 0.5)
+    cands = [((256, 128, 64), 3, 4, 4, 256, 1), ((256, 256, 64), 2, 4, 8, 256, 1)]
+    M = N = K = 8192
+    with_table = optimize(M, N, K, params, cands, "time", table=table)
+    assert {(tuple(r["tile"]), r["consumer_waves"]) for r in with_table} == {((256, 128, 64), 4),
+                                                                          ((256, 256, 64), 8)}
+    eight = next(r for r in with_table if r["consumer_waves"] == 8)
+    assert eight["costs"] == "table" and eight["split"] == 1
+    # 256 x 256 tiles: 1024 tiles in 4 rounds of 128 K-iterations at t_math = 1.4 us dominate
+    assert eight["time_us"] > 4 * 128 * 1.4
+    without = optimize(M, N, K, params, cands, "time")
+    assert [r["consumer_waves"] for r in without] == [4]
