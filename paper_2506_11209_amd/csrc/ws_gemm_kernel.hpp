@@ -157,11 +157,15 @@ __device__ __forceinline__ uint32_t cycles32() {
 
 // XOR swizzle of the 16-byte chunks of A-tile row r.  It depends on r & 31
 // only, so rows 32 apart share it and the consumer can fold whole 32-row
-// blocks into instruction offsets.  Rows 0..15 read by one ds_read_b128 fall
-// on distinct 16-byte bank groups (for both 128- and 256-byte bank rows).
+// blocks into instruction offsets.  The operand read (lane l: row l & 31,
+// chunk l / 32, or that chunk XOR 2 for the next k-step) is free of LDS bank
+// conflicts with these choices, as measured with SQ_LDS_BANK_CONFLICT on
+// gfx950 at every block and slot base the kernels use; at TK = 32,
+// ((r >> 1) ^ (r >> 3)) & 3 and (r >> 1) & 3 cost four conflict cycles per
+// read and no swizzle twelve.
 template <int TK>
 __host__ __device__ constexpr int swz_a(int r) {
-  if constexpr (TK == 32) return ((r >> 1) ^ (r >> 3)) & 3;
+  if constexpr (TK == 32) return (r ^ (r >> 2)) & 3;
   else if constexpr (TK == 64) return (r ^ ((r >> 3) & 1)) & 7;
   else return r & 15;
 }

@@ -54,7 +54,7 @@ def blocks():
 def swz_a(tk, r):
     """The kernels' XOR swizzle of A-tile row r (ws_gemm_kernel.hpp, swz_a)."""
     if tk == 32:
-        return ((r >> 1) ^ (r >> 3)) & 3
+        return (r ^ (r >> 2)) & 3
     if tk == 64:
         return (r ^ ((r >> 3) & 1)) & 7
     return r & 15
