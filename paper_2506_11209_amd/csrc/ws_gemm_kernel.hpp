@@ -455,6 +455,29 @@ enum KernelMode {
   kModeGemm = 0, kModeLoadA = 1, kModeLoadB = 2, kModeMath = 3, kModeEpilogue = 4, kModeLoadAB = 5
 };
 
+typedef __attribute__((ext_vector_type(4))) int i32x4_t;
+
+// Producer loads and the epilogue's stores go through a raw buffer resource
+// over a tile panel: the base sits in SGPRs and each lane adds a 32-bit byte
+// offset (panel offsets stay below 2^31, checked by the plan), so an access
+// needs no 64-bit address arithmetic on the vector ALU of a SIMD whose other
+// waves issue MFMAs.  Word 3 of the descriptor: data format
+// 32 bits (field at bits 15-18 = 4), every other field zero (no swizzle, no
+// index stride); the record count is the largest, so no offset is clipped.
+constexpr int kRawBufferWord3 = 0x00020000;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, -1, kRawBufferWord3);
+}
+// Cache-policy operand of the raw buffer builtins that marks an access
+// non-temporal (the `nt` bit).
+constexpr int kBufferNonTemporal = 2;
+__device__ __forceinline__ i32x4_t panel_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(i32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 0));
+}
+// 16 bytes per lane straight into LDS: lane l's bytes land at dst + 16 l.
+__device__ __forceinline__ void panel_load16_lds(__amdgpu_buffer_rsrc_t r, WSG_LDS void* dst, uint32_t byte_off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, byte_off, 0, 0, 0);
+}
 // Epilogue: the fp32 tile of consumer wave (wm, wn) to C.  acc[mb][nb][e] is
 // row 8(e/4) + 4(lane/32) + e%4, column lane%32 of the 32x32 block.  The row
 // pitch is made opaque so that the address arithmetic stays here instead of
@@ -555,18 +578,23 @@ __device__ __forceinline__ void store_tile(const KernelArgs& args, const f32x16_
   } else {
     uint32_t ldc = (uint32_t)args.N * 4u;
     asm volatile("" : "+s"(ldc));
-    char* cbase = (char*)args.C +
-                  (((int64_t)ti * TM + wm * WM) * (int64_t)args.N + (int64_t)tj * TN + wn * WN) * 4;
+    const char* cbase = (const char*)args.C +
+                        (((int64_t)ti * TM + wm * WM) * (int64_t)args.N + (int64_t)tj * TN + wn * WN) * 4;
+    // the wave tile's rows lie below T_M * N * 4 < 2^31 bytes from cbase
+    const __amdgpu_buffer_rsrc_t crs = panel_rsrc(cbase);
     const uint32_t lane_off = (uint32_t)(4 * (lane >> 5)) * ldc + (uint32_t)(lane & 31) * 4u;
 #pragma unroll
     for (int mb = 0; mb < BM; ++mb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int dr = mb * 32 + 8 * (e >> 2) + (e & 3);
-        char* rowp = cbase + (uint32_t)dr * ldc;
+        const uint32_t row_off = (uint32_t)(mb * 32 + 8 * (e >> 2) + (e & 3)) * ldc;  // wave-uniform
 #pragma unroll
-        for (int nb = 0; nb < BN; ++nb)  // non-temporal: C is not read again here, the panels are
-          __builtin_nontemporal_store(acc[mb][nb][e], (float*)(rowp + lane_off + nb * 128));
+        for (int nb = 0; nb < BN; ++nb) {  // non-temporal: C is not read again here, the panels are
+          // copy the element out first: a bit cast of a vector element lvalue reads element 0
+          const float v = acc[mb][nb][e];
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), crs, (int)(lane_off + nb * 128),
+                                                (int)row_off, kBufferNonTemporal);
+        }
       }
   }
 }
@@ -579,26 +607,6 @@ __device__ __forceinline__ int first_slot(const KernelArgs& args) {
   return args.xcd_remap ? xcd_slot(blockIdx.x, G) : (int)blockIdx.x;
 }
 
-typedef __attribute__((ext_vector_type(4))) int i32x4_t;
-
-// Producer loads go through a raw buffer resource over the K-iteration's
-// tile panel: the base sits in SGPRs and each lane adds a 32-bit byte offset
-// (panel offsets stay below 2^31, checked by the plan), so a load needs no
-// 64-bit address arithmetic on the vector ALU of a SIMD whose other waves
-// issue MFMAs.  Word 3 of the descriptor: data format
-// 32 bits (field at bits 15-18 = 4), every other field zero (no swizzle, no
-// index stride); the record count is the largest, so no offset is clipped.
-constexpr int kRawBufferWord3 = 0x00020000;
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc(const void* base) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, -1, kRawBufferWord3);
-}
-__device__ __forceinline__ i32x4_t panel_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
-  return __builtin_bit_cast(i32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 0));
-}
-// 16 bytes per lane straight into LDS: lane l's bytes land at dst + 16 l.
-__device__ __forceinline__ void panel_load16_lds(__amdgpu_buffer_rsrc_t r, WSG_LDS void* dst, uint32_t byte_off) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, byte_off, 0, 0, 0);
-}
 // Events of one kind that a producer wave stores into its workgroup's trace
 // record, batched: lane k of `vals` holds the event of K-iteration base + k
 // (events arrive for consecutive K-iterations), and 64 of them go out in one
