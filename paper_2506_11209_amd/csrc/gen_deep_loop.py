@@ -48,9 +48,10 @@ OUT = os.path.join(HERE, "ws_deep_loop.inc")
 # (four consumer waves in a 2 x 2 grid).  Its fixed fragment registers make a
 # kernel take all of a wave's registers (256 with one producer group, 168
 # with two).  Left out because they measured slower with it (8192^3):
-# 128x128x32 1:1 (6 %; its compiler-scheduled kernel needs 111 VGPRs and
-# runs two workgroups per CU), 64x128x32 and 128x64x32 1:1 (7-8 %); the
-# 2:1 kernels of the largest tiles run the register-lean consumer.
+# 128x128x32 1:1 (6 %: one workgroup per CU where the compiler-scheduled
+# kernel runs two; it takes the register-lean roll loop below, which keeps
+# two), 64x128x32 and 128x64x32 1:1 (7-8 %); the 2:1 kernels of the largest
+# tiles run the register-lean consumer.
 # (TM, TN, TK, NC, NP): NP producer waves.  Four producer waves serve both
 # the 1:1 arrangement and the 2:1 one with two groups of two (the consumer
 # side is the same); eight are the 2:1 arrangement with two groups of four.
@@ -372,11 +373,14 @@ struct DeepLoop<%(tm)d, %(tn)d, %(tk)d, %(nc)d, %(np)d, %(bf16)s> {
 
 
 # ---------------------------------------------------------------------------
-# Register-lean loop for eight consumer waves (two per SIMD) next to four
-# producer waves: twelve waves leave 168 registers a wave, 128 of them the
-# 128 x 64 accumulator, so each fragment is single-buffered and refilled right
-# after its last MFMA of the k-step; the second consumer wave on the SIMD
-# keeps the matrix core busy while one waits for a read.
+# Register-lean loop for two consumer waves per SIMD.  Eight consumer waves
+# (2 x 4 grid) next to four producer waves: twelve waves leave 168 registers a
+# wave, 128 of them the 128 x 64 accumulator.  Four consumer waves (2 x 2
+# grid) next to four producer waves at 128 x 128 x 32: the kernel is held to
+# 128 registers a wave so that two workgroups share a CU (sixteen waves), 64
+# of them the 64 x 64 accumulator.  Either way each fragment is single-buffered
+# and refilled right after its last MFMA of the k-step; the other consumer
+# wave on the SIMD keeps the matrix core busy while one waits for a read.
 #
 # Per k-step t (N-major MFMA order, B fragment nb used by BM consecutive
 # MFMAs, A fragment mb by MFMAs mb and BM + mb):
@@ -388,20 +392,22 @@ struct DeepLoop<%(tm)d, %(tn)d, %(tk)d, %(nc)d, %(np)d, %(bf16)s> {
 # the k-step bits for A, the slot's byte delta for both.
 # ---------------------------------------------------------------------------
 # (TM, TN, TK, NC, NP)
-ROLL_CONFIGS = [(256, 256, 64, 8, 4), (256, 256, 32, 8, 4)]
+ROLL_CONFIGS = [(256, 256, 64, 8, 4), (256, 256, 32, 8, 4), (128, 128, 32, 4, 4)]
 
 
 class RollCfg:
     def __init__(self, tm, tn, tk, nc, np):
-        assert nc == 8 and np == 4 and tk in (32, 64)
+        assert nc in (4, 8) and np == 4 and tk in (32, 64)
         self.tm, self.tn, self.tk, self.nc, self.np = tm, tn, tk, nc, np
         self.ks = tk // 16
-        self.wm, self.wn = tm // 2, tn // 4
+        self.wgn = 4 if nc == 8 else 2                # consumer grid columns (two rows)
+        self.wm, self.wn = tm // 2, tn // self.wgn
         self.bm, self.bn = self.wm // 32, self.wn // 32
         self.nq = tn // 16
         self.a_bytes = tm * tk * 2
         self.stage = self.a_bytes + tk * tn * 2
-        self.vgprs = 168
+        # registers a wave: 168 with twelve waves, 128 with two workgroups of eight
+        self.vgprs = 168 if nc == 8 else 128
         self.frag_regs = 4 * (self.bm + self.bn)
         self.frag_base = self.vgprs - self.frag_regs
         assert self.bn == 2 and self.bm * self.bn * 16 + self.frag_regs <= self.vgprs - 8
@@ -719,7 +725,7 @@ def generate() -> str:
     for t in CONFIGS:
         for bf16 in (True, False):
             parts.append(gen_struct(Cfg(*t), bf16))
-    parts += ["// The K loop of one output tile for eight consumer waves (consumer_roll).",
+    parts += ["// The K loop of one output tile for two consumer waves per SIMD (consumer_roll).",
               "template <int TM, int TN, int TK, int NC, int NP, bool BF16>",
               "struct RollLoop {",
               "  static constexpr bool kAvailable = false;",

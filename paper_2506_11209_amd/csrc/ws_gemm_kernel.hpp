@@ -834,7 +834,8 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
   constexpr int B_PER = DO_B ? G::B_INSTR / B_GROUP : 0;
   constexpr int LOADS = A_PER + B_PER;
   // VGPRs for staged tiles: what the consumers' allocation leaves (256 a wave
-  // with eight waves, 168 with twelve)
+  // with eight waves, 168 with twelve; the 128 x 128 x 32 kernel held to 128
+  // registers stages its cap of six K-iterations in 96)
   constexpr int STAGE_VGPRS = (G::NW <= 8) ? 152 : (NC == 8 ? 128 : 96);
   constexpr int L0 = STAGE_VGPRS / (4 * LOADS);
   constexpr int L1 = (63 / LOADS) < L0 ? (63 / LOADS) : L0;
@@ -1341,11 +1342,13 @@ __device__ __forceinline__ void consumer_deep(const KernelArgs& args, WSG_LDS ch
 }
 
 // ---------------------------------------------------------------------------
-// Consumer of the eight-consumer arrangement (two consumer waves per SIMD,
-// 2 x 4 grid of 128 x 64 wave tiles, next to four producer waves): the K loop
-// of a tile is the generated RollLoop block (ws_deep_loop.inc).  Its
-// fragments are single-buffered and refilled right after their last MFMA of
-// the k-step; the other consumer wave of the SIMD covers the read latency.
+// Consumer with two consumer waves per SIMD: the eight-consumer arrangement
+// (2 x 4 grid of 128 x 64 wave tiles next to four producer waves) and the
+// four-consumer 128 x 128 x 32 kernel held to 128 registers a wave (2 x 2
+// grid of 64 x 64 wave tiles, two workgroups per CU).  The K loop of a tile is
+// the generated RollLoop block (ws_deep_loop.inc).  Its fragments are
+// single-buffered and refilled right after their last MFMA of the k-step; the
+// other consumer wave of the SIMD covers the read latency.
 // ---------------------------------------------------------------------------
 template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
 __device__ __forceinline__ void consumer_roll(const KernelArgs& args, WSG_LDS char* smem, int cw,
@@ -1627,8 +1630,18 @@ __global__ void __launch_bounds__(256) ws_scale_kernel(void* C, int64_t n, float
 template <int UNUSED = 0>
 __global__ void __launch_bounds__(1024) ws_empty_kernel(KernelArgs) {}
 
+// Waves per SIMD a kernel's register allocation must leave room for: the
+// four-consumer roll loop holds its kernel to 128 registers a wave so that two
+// workgroups of eight waves share a CU; every other kernel is sized for one
+// workgroup (what the compiler assumes without the bound).
+template <int TM, int TN, int TK, int NC, int NPW, bool BF16, bool GENERAL>
+constexpr int kernel_waves_per_simd() {
+  return (NC == 4 && !GENERAL && RollLoop<TM, TN, TK, NC, NPW, BF16>::kAvailable) ? 4 : (NC + NPW + 3) / 4;
+}
+
 template <int TM, int TN, int TK, int NC, int NPW, int SPLIT, bool BF16, bool TRACE, int MODE, bool GENERAL>
-__global__ void __launch_bounds__((NC + NPW) * 64) ws_gemm_kernel(KernelArgs args) {
+__global__ void __launch_bounds__((NC + NPW) * 64, (kernel_waves_per_simd<TM, TN, TK, NC, NPW, BF16, GENERAL>()))
+    ws_gemm_kernel(KernelArgs args) {
   using G = Cfg<TM, TN, TK, NC, NPW, SPLIT, BF16>;
   extern __shared__ __attribute__((aligned(1024))) char smem_generic[];
   WSG_LDS char* smem = (WSG_LDS char*)smem_generic;
@@ -1645,7 +1658,8 @@ __global__ void __launch_bounds__((NC + NPW) * 64) ws_gemm_kernel(KernelArgs arg
       consumer_epilogue_only<TM, TN, TK, NC, NPW, SPLIT, BF16>(args, wave, lane);
     } else if constexpr (!GENERAL && (MODE == kModeGemm || MODE == kModeMath) &&
                          RollLoop<TM, TN, TK, NC, NPW, BF16>::kAvailable) {
-      // Eight consumer waves: the generated register-lean K loop (and its
+      // Two consumer waves per SIMD (eight consumer waves, or four with two
+      // workgroups per CU): the generated register-lean K loop (and its
       // event-traced twin).
       consumer_roll<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
     } else if constexpr (G::NW > 8 && G::BM * G::BN >= 8) {

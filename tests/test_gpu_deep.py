@@ -1,8 +1,9 @@
 """The generated asm K loops (ws_deep_loop.inc) in every configuration that
 runs them: the deep-prefetch consumer of four consumer waves (the
 generator's list: four or eight producer waves, one or two producer groups,
-TK = 64 and 32) and the register-lean loop of eight consumer waves (256 x 256
-tiles, four producer waves in one or two groups).  Their prologue, loop
+TK = 64 and 32) and the register-lean loop of two consumer waves per SIMD
+(eight consumer waves at 256 x 256, four at 128 x 128 x 32 with two
+workgroups per CU; four producer waves in one or two groups).  Their prologue, loop
 bodies and last k-steps (1-8 K-iterations per tile; TK = 32 deep-consumer
 tiles with an odd count take the compiler-scheduled consumer instead), slot
 wrap-around at every ring depth that fits, two output tiles per workgroup,
@@ -88,7 +89,7 @@ def run_and_check(M, N, K, tile, stages, dtype="bf16", load_path="registers", de
 def test_k_iterations_and_ring_depths(cfg, iters, load_path):
     tm, tn, tk, nc, np_, split = cfg
     tile = (tm, tn, tk)
-    M, N, K = 16 * tm, 32 * tn, iters * tk  # 512 tiles: two or more per workgroup
+    M, N, K = 32 * tm, 32 * tn, iters * tk  # 1024 tiles: two or more per workgroup (up to 2 per CU)
     for stages in range(2, min(4, max_stages(tile)) + 1):
         log("case deep %s nc=%d np=%d %d:1 S=%d P=%d %s" % (tile, nc, np_, split, iters, stages, load_path))
         info = run_and_check(M, N, K, tile, stages, load_path=load_path, seed=100 * iters + stages,

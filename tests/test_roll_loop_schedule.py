@@ -1,5 +1,6 @@
-"""Static check of the generated K loop of the eight-consumer arrangement
-(RollLoop in paper_2506_11209_amd/csrc/ws_deep_loop.inc), CPU only.
+"""Static check of the generated K loop for two consumer waves per SIMD
+(RollLoop in paper_2506_11209_amd/csrc/ws_deep_loop.inc: eight consumer waves
+in a 2 x 4 grid, or four in a 2 x 2 grid at 128 x 128 x 32), CPU only.
 
 The asm text of every configuration is executed by a small interpreter: the
 scalar and address arithmetic run on concrete values for several lanes of
@@ -72,7 +73,8 @@ class Lane:
 
     def __init__(self, c, cw, lane):
         self.c, self.cw, self.lane = c, cw, lane
-        self.wm, self.wn = cw // 4, cw % 4
+        grid_n = 4 if c.nc == 8 else 2  # the kernel's consumer grid: two rows of NC / 2 waves
+        self.wm, self.wn = cw // grid_n, cw % grid_n
         r = self.wm * c.wm + (lane & 31)
         self.a_off0 = r * c.tk * 2 + (((lane >> 5) ^ swz_a(c.tk, r)) << 4)
         g = lane >> 4
@@ -346,7 +348,8 @@ def iter_counts():
 
 
 def lanes_of(c):
-    return [Lane(c, cw, ln) for cw in (0, 3, 5) for ln in (0, 1, 15, 16, 31, 32, 47, 63)]
+    waves = (0, 3, 5) if c.nc == 8 else (0, 1, 3)  # both grid rows, several columns
+    return [Lane(c, cw, ln) for cw in waves for ln in (0, 1, 15, 16, 31, 32, 47, 63)]
 
 
 CASES = [(k, S, polls, P) for k in sorted(blocks()) for S in iter_counts() for polls in (0, 1, 2)
@@ -421,4 +424,4 @@ def test_checker_catches_a_weakened_wait(key):
                 sim.run(bad)
                 found |= bool(sim.errors)
         caught += found
-    assert total > 10 and caught >= total - 2, (caught, total)
+    assert total >= 10 and caught >= total - 2, (caught, total)
