@@ -16,7 +16,8 @@
 //  * Roles are chosen per wavefront from the wave index, so no wave diverges
 //    (Section 1.2).  Waves [0, NC) are consumers, waves [NC, NC + NP) are
 //    producers.  With NC = 4 the consumers sit one per SIMD and tile the
-//    output block 2 x 2.
+//    output block 2 x 2; with NC = 8 (256 x 256 tiles, four producer waves)
+//    two per SIMD, 2 x 4.
 //  * Producers move a tile in 16-byte chunks, 1 KiB per wave instruction,
 //    either staged through VGPRs several K-iterations ahead
 //    (buffer_load_dwordx4, then ds_write_b128 once the slot is free; the
@@ -30,12 +31,16 @@
 //  * Consumers read operands with ds_read_b128 (A, K-contiguous) and
 //    ds_read_b64_tr_b16 (B, N-contiguous, transposed by the read) and
 //    accumulate with v_mfma_f32_32x32x16_{bf16,f16} in fp32.  In the plain
-//    kernel of most tiles (the list is in gen_deep_loop.py: 1:1 tiles of
-//    64x128 and up, 2:1 tiles up to 128x128) the K loop of a tile is a
-//    generated asm block (consumer_deep, ws_deep_loop.inc) that keeps the
-//    reads of the next k-steps in flight behind the MFMAs; the other shapes,
-//    the general variant, the event-traced twin and the register-lean 2:1
-//    variants of the largest tiles run compiler-scheduled consumers.
+//    kernels the K loop of a tile is a generated asm block (ws_deep_loop.inc,
+//    configurations listed in gen_deep_loop.py): with two consumer waves per
+//    SIMD (eight consumer waves, or four at 128 x 128 x 32 with two
+//    workgroups per CU) the register-lean roll loop (consumer_roll, also in
+//    the event-traced twin), with one the deep-prefetch loop that keeps the
+//    reads of the next three k-steps in flight behind the MFMAs
+//    (consumer_deep: 1:1 tiles of 64x128 and up at TK = 64 and 128x256x32,
+//    2:1 tiles up to 128x128).  The other shapes, the general variant, the
+//    traced twins of the deep-prefetch kernels and the 2:1 kernels of the
+//    largest four-consumer tiles run compiler-scheduled consumers.
 //  * The grid is persistent: at most one workgroup per CU slot, each walking
 //    output tiles in dispatch rounds (Section 2.1, "Wave").  The tile order
 //    places the tiles that run at the same time on one XCD next to each
