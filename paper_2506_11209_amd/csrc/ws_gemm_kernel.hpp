@@ -968,12 +968,15 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
       const uint32_t slot = ring_slot(q, P);
       if (ring_use(q, P) > 0) {
         const uint32_t need = ring_empty_target(q, P, NC);
-        if ((int32_t)(lds_read_now(&empty[slot]) - need) < 0) {
-          if (!wait_counter(&empty[slot], need, abort_flag, args.spin_limit, args.err)) {
-            wait_vmcnt<0>();
-            return;
-          }
-        }
+        // No early exit when the wait fails (workgroup aborted, or this
+        // wait timed out and raised the abort): the wave runs its remaining
+        // K-iterations without waiting (every later wait sees the abort flag
+        // at once) and leaves at the loop's end.  A return from inside the
+        // loop would join the loop header in the compiler's control flow,
+        // and its wait-count analysis would then drain every load in flight
+        // at the first register stage of each pass through the stages.
+        if ((int32_t)(lds_read_now(&empty[slot]) - need) < 0)
+          (void)wait_counter(&empty[slot], need, abort_flag, args.spin_limit, args.err);
       }
       debug_delay(args.producer_delay);
       compiler_fence();

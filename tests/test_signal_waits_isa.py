@@ -1,4 +1,4 @@
-"""The slot signals in the built kernels' machine code (CPU only).
+"""The slot signals and producer waits in the built kernels' machine code (CPU only).
 
 A consumer releases a slot with `s_waitcnt lgkmcnt(n)` followed by
 `ds_add_u32`, where n counts the LDS reads issued after the last read of the
@@ -10,7 +10,9 @@ checks the stronger property on the compiled code itself, so that the
 release does not depend on that argument at all: at every `ds_add_u32` whose
 nearest wait is lgkmcnt(n) with n > 0, no scalar load may still be in flight
 on any path into that wait (a scalar load is known complete only after an
-lgkmcnt(0) wait).
+lgkmcnt(0) wait).  A second check covers the register-staged producers'
+global-load waits: the wait before a slot write never drains the loads of the
+K-iterations staged behind it.
 
 The code is read from the gfx950 code objects of paper_2506_11209_amd/
 libwsgemm.so (built here from source) and disassembled with the ROCm
@@ -152,19 +154,68 @@ def test_the_analysis_flags_a_scalar_load_in_flight():
     assert unsafe_signals(0, unguarded)[1][0][1] == "no LDS wait before the signal"
 
 
-@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
-@pytest.mark.skipif(not os.path.exists(OBJDUMP), reason="llvm-objdump not found")
-def test_no_signal_waits_on_a_count_that_a_scalar_load_shares():
+_needs_lib = [pytest.mark.skipif(not os.path.exists(LIB), reason="library not built"),
+              pytest.mark.skipif(not os.path.exists(OBJDUMP), reason="llvm-objdump not found")]
+
+
+@pytest.fixture(scope="module")
+def library_code():
+    """[(kernel, start, instructions)] of every kernel in the built library."""
     with open(LIB, "rb") as f:
         lib = f.read()
+    return [(name, start, ins) for co in kc._code_objects(lib) for name, (start, ins) in disassemble(co).items()]
+
+
+@_needs_lib[0]
+@_needs_lib[1]
+def test_no_signal_waits_on_a_count_that_a_scalar_load_shares(library_code):
     kernels = signals = younger = 0
     problems = []
-    for co in kc._code_objects(lib):
-        for name, (start, ins) in disassemble(co).items():
-            checked, bad = unsafe_signals(start, ins)
-            kernels += 1
-            signals += checked
-            younger += sum(1 for (_, mn, ops, _) in ins if mn == "s_waitcnt" and (lgkm_of(ops) or 0) > 0)
-            problems += [(name, a, why) for a, why in bad]
+    for name, start, ins in library_code:
+        checked, bad = unsafe_signals(start, ins)
+        kernels += 1
+        signals += checked
+        younger += sum(1 for (_, mn, ops, _) in ins if mn == "s_waitcnt" and (lgkm_of(ops) or 0) > 0)
+        problems += [(name, a, why) for a, why in bad]
     assert kernels > 400 and signals > 1000 and younger > 0
     assert not problems, problems[:10]
+
+
+def staged_write_waits(ins):
+    """vmcnt of the wait guarding each ds_write_b128 (the register-staged
+    producers' slot writes), in program order."""
+    out = []
+    for i, (_, mn, _, _) in enumerate(ins):
+        if mn != "ds_write_b128":
+            continue
+        j = i - 1
+        while j >= 0 and ins[j][1] != "s_waitcnt" and not ins[j][1].startswith("ds_write"):
+            j -= 1
+        if j >= 0 and ins[j][1] == "s_waitcnt":
+            m = re.search(r"vmcnt\((\d+)\)", ins[j][2])
+            if m:
+                out.append(int(m.group(1)))
+    return out
+
+
+@_needs_lib[0]
+@_needs_lib[1]
+def test_register_staged_producers_never_drain_their_staged_loads(library_code):
+    """A register-staged producer keeps several K-iterations of loads in
+    flight and writes the oldest one to its slot: the wait before that write
+    must leave the newer iterations' loads outstanding.  A wait for every
+    load (vmcnt(0)) there empties the pipeline and exposes a full memory
+    latency; the compiler placed one at the first register stage of every
+    pass through the stages while the wait loop could leave the loop early
+    (10 % of the load-only time at 16384 x 256 x 8192)."""
+    kernels, drained = 0, []
+    for name, _, ins in library_code:
+        if "ws_gemm_kernel" not in name:
+            continue
+        waits = staged_write_waits(ins)
+        if waits:
+            kernels += 1
+            if min(waits) == 0:
+                drained.append((name, waits[:16]))
+    assert kernels > 300
+    assert not drained, drained[:5]
