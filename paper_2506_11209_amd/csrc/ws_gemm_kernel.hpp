@@ -228,6 +228,35 @@ __device__ __forceinline__ void lds_signal(WSG_LDS uint32_t* p) {
 #endif
 }
 
+// signal() of the counter at p, together with a read of the counter at
+// `peek`: the read goes out before the wait that the signal needs anyway (for
+// the wave's own LDS writes), so it costs no LDS round trip of its own.
+// Returns the value read (wave-uniform); the counters are monotonic, so a
+// value that already satisfies a later wait stays valid.
+__device__ __forceinline__ uint32_t lds_signal_peek(WSG_LDS uint32_t* p, WSG_LDS uint32_t* peek) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const uint32_t addr = (uint32_t)(uintptr_t)p;
+  const uint32_t paddr = (uint32_t)(uintptr_t)peek;
+  const uint32_t one = 1u;
+  uint64_t saved;
+  uint32_t v;
+  asm volatile(
+      "ds_read_b32 %1, %3\n\t"
+      "s_waitcnt lgkmcnt(0)\n\t"
+      "s_mov_b64 %0, exec\n\t"
+      "s_mov_b64 exec, 1\n\t"
+      "ds_add_u32 %2, %4\n\t"
+      "s_mov_b64 exec, %0"
+      : "=&s"(saved), "=&v"(v)
+      : "v"(addr), "v"(paddr), "v"(one)
+      : "memory");
+  return __builtin_amdgcn_readfirstlane(v);
+#else
+  *p += 1;
+  return *peek;
+#endif
+}
+
 // signal() when `enable` (wave-uniform) is non-zero, as one asm block, so
 // the caller's control flow gets no join.
 template <int YOUNGER = 0>
@@ -960,24 +989,26 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
 #pragma unroll
   for (int u = 0; u < L; ++u) issue(u);
 
+  // Slot of the next K-iteration to write, the empty[] value its use needs
+  // (0 for a slot's first use), and the value of that counter read with the
+  // previous signal: when the consumers are ahead it already satisfies the
+  // wait, and the wave skips an LDS round trip.
+  uint32_t w_slot = 0, w_need = 0, seen = 0;
   for (uint32_t q0 = 0; q0 < total; q0 += L) {
 #pragma unroll
     for (int u = 0; u < L; ++u) {
       const uint32_t q = q0 + u;
       if (q < total) {
-      const uint32_t slot = ring_slot(q, P);
-      if (ring_use(q, P) > 0) {
-        const uint32_t need = ring_empty_target(q, P, NC);
-        // No early exit when the wait fails (workgroup aborted, or this
-        // wait timed out and raised the abort): the wave runs its remaining
-        // K-iterations without waiting (every later wait sees the abort flag
-        // at once) and leaves at the loop's end.  A return from inside the
-        // loop would join the loop header in the compiler's control flow,
-        // and its wait-count analysis would then drain every load in flight
-        // at the first register stage of each pass through the stages.
-        if ((int32_t)(lds_read_now(&empty[slot]) - need) < 0)
-          (void)wait_counter(&empty[slot], need, abort_flag, args.spin_limit, args.err);
-      }
+      const uint32_t slot = w_slot;
+      // No early exit when the wait fails (workgroup aborted, or this wait
+      // timed out and raised the abort): the wave runs its remaining
+      // K-iterations without waiting (every later wait sees the abort flag
+      // at once) and leaves at the loop's end.  A return from inside the
+      // loop would join the loop header in the compiler's control flow, and
+      // its wait-count analysis would then drain every load in flight at the
+      // first register stage of each pass through the stages.
+      if ((int32_t)(seen - w_need) < 0)
+        (void)wait_counter(&empty[slot], w_need, abort_flag, args.spin_limit, args.err);
       debug_delay(args.producer_delay);
       compiler_fence();
       WSG_LDS char* base = smem + kHeaderBytes + slot * G::STAGE + lane16;
@@ -997,7 +1028,12 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
         stamps.issued(q, t_issue[u], &full[kStampIssueA + slot], &full[kStampIssueB + slot]);
         stamps.landed(q, t_now, &full[kStampLandA + slot], &full[kStampLandB + slot]);
       }
-      lds_signal(&full[slot]);  // waits for the LDS writes, then signals
+      if (++w_slot == P) {
+        w_slot = 0;
+        w_need += NC;
+      }
+      // waits for the LDS writes, signals, and reads the next slot's empty[]
+      seen = lds_signal_peek(&full[slot], &empty[w_slot]);
       }
       issue(u);  // refill this register stage with K-iteration q + L
     }

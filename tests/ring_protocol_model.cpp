@@ -37,6 +37,8 @@
 //   PLANT_DROP_SIGNAL    producer 0 skips its signal of K-iteration T/2
 //   PLANT_SHORT_DRAIN    (with LAG) a blocked producer signals pending
 //                        K-iterations only up to q - P
+//   PLANT_PEEK_WRONG_SLOT the counter read with a signal is the signalled
+//                        slot's, not the next one's
 #include <atomic>
 #include <chrono>
 #include <cstdint>
@@ -94,17 +96,34 @@ bool wait_for(Ring& r, std::atomic<uint32_t>& ctr, uint32_t target) {
   return true;
 }
 
+// The register-staged producer: it walks the slots incrementally and, with
+// each signal, reads the empty[] counter of the slot it writes next; it
+// waits on that slot only when the value read does not already reach the
+// target (the counters are monotonic).
 void producer(Ring& r, uint32_t p) {
+  uint32_t w_slot = 0, w_need = 0, seen = 0;
   for (uint32_t q = 0; q < r.T; ++q) {
-    const uint32_t slot = wsg::ring_slot(q, r.P);
-    if (wsg::ring_use(q, r.P) > 0 && !wait_for(r, r.empty[slot], wsg::ring_empty_target(q, r.P, r.NC)))
+    const uint32_t slot = w_slot;
+    if (slot != wsg::ring_slot(q, r.P) || w_need != wsg::ring_empty_target(q, r.P, r.NC)) {
+      r.mismatches.fetch_add(1);  // the incremental walk disagrees with the closed forms
       return;
+    }
+    if ((int32_t)(seen - w_need) < 0 && !wait_for(r, r.empty[slot], w_need)) return;
     uint64_t* d = r.share(slot, p);
     for (int c = 0; c < kChunks; ++c) d[c] = tag(q, p, c);
+    if (++w_slot == r.P) {
+      w_slot = 0;
+      w_need += r.NC;
+    }
 #ifdef PLANT_DROP_SIGNAL
     if (p == 0 && q == r.T / 2) continue;
 #endif
     r.full[slot].fetch_add(1, std::memory_order_release);
+#ifdef PLANT_PEEK_WRONG_SLOT
+    seen = r.empty[slot].load(std::memory_order_acquire);
+#else
+    seen = r.empty[w_slot].load(std::memory_order_acquire);
+#endif
   }
 }
 

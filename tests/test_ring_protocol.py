@@ -5,8 +5,9 @@ built with g++ and ThreadSanitizer, over the ring arithmetic the kernels use
 The correct protocol must run every configuration without a data race, a
 wrong tag or a timeout; each planted mistake must be caught: a slot released
 before it is read or read one signal early races (ThreadSanitizer) and
-returns wrong tags, and a dropped signal ends in the watchdog's timeout
-instead of a hang.
+returns wrong tags, a producer that skips its wait on a counter value read
+from the wrong slot races, and a dropped signal ends in the watchdog's
+timeout instead of a hang.
 
 The deferred-signal mode (the LDS-DMA producer, which signals a K-iteration
 only once later ones are in flight, against consumers that check K-iteration
@@ -32,7 +33,8 @@ TSAN_RACE_STATUS = 66  # ThreadSanitizer's exit status when it reported a race
 def models(tmp_path_factory):
     out = tmp_path_factory.mktemp("ring_model")
     built = {}
-    for plant in ("", "PLANT_EARLY_RELEASE", "PLANT_EARLY_READ", "PLANT_DROP_SIGNAL", "PLANT_SHORT_DRAIN"):
+    for plant in ("", "PLANT_EARLY_RELEASE", "PLANT_EARLY_READ", "PLANT_DROP_SIGNAL", "PLANT_SHORT_DRAIN",
+                  "PLANT_PEEK_WRONG_SLOT"):
         exe = str(out / ("model_" + (plant or "ok")))
         cmd = ["g++", "-std=c++17", "-O1", "-g", "-pthread", "-fsanitize=thread", "-I" + INCLUDE, SOURCE,
                "-o", exe]
@@ -81,6 +83,14 @@ def test_dropped_signal_times_out_instead_of_hanging(models, P, NP, NC):
     rc, out = run(models["PLANT_DROP_SIGNAL"], P, NP, NC, 2000, limit_ms=300)
     assert rc == 2, out
     assert "ThreadSanitizer" not in out, out
+
+
+@pytest.mark.parametrize("P,NP,NC", [(2, 4, 4), (3, 8, 4), (4, 4, 8)])
+def test_reading_the_wrong_slot_with_the_signal_is_caught(models, P, NP, NC):
+    # the signalled slot's counter says nothing about the next slot's
+    # previous use: the producer overwrites it while consumers still read it
+    rc, out = run(models["PLANT_PEEK_WRONG_SLOT"], P, NP, NC, 2000)
+    assert rc == TSAN_RACE_STATUS and "data race" in out, out
 
 
 # the LDS-DMA producer's lags: 1 for two slots, P - 2 beyond; 0 and larger
