@@ -65,6 +65,28 @@ def traffic_for(point_key: str, point=DEFAULT_POINT, dtype="bf16", workload=WORK
     return None
 
 
+def copy_bandwidth(gib: float = 1.0, reps: int = 10) -> float:
+    """Measured device copy bandwidth of this GPU in GB/s (read plus write
+    bytes per second of a `gib` GiB tensor copy, HIP events around `reps`
+    copies after a warm-up): the practical HBM reference beside the 8 TB/s
+    peak for workloads below the ridge point."""
+    import torch
+    n = int(gib * (1 << 30)) // 2
+    src = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    for _ in range(reps):
+        dst.copy_(src)
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / reps
+    del src, dst
+    return 2.0 * 2 * n / (ms * 1e-3) / 1e9
+
+
 def host_cpu() -> dict:
     """CPU model and thread counts of this host."""
     model = "unknown"
@@ -244,6 +266,11 @@ def main():
     if a.cold_flush_mib > 0:
         out["cold_flush_mib"] = a.cold_flush_mib  # value includes the flushes; roofline does not
     g.close()
+    if bound == "hbm":
+        # against what this machine's HBM sustains in practice, measured after the timed region
+        cbw = copy_bandwidth()
+        out["roofline"]["copy_gbs"] = round(cbw, 1)
+        out["roofline"]["frac_of_copy"] = round(achieved / cbw, 4)
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl)
     print(json.dumps(out), flush=True)
