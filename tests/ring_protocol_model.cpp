@@ -116,9 +116,9 @@ void producer(Ring& r, uint32_t p) {
       w_need += r.NC;
     }
 #ifdef PLANT_DROP_SIGNAL
-    if (p == 0 && q == r.T / 2) continue;
+    if (!(p == 0 && q == r.T / 2))  // only the signal goes missing; the peek below still runs
 #endif
-    r.full[slot].fetch_add(1, std::memory_order_release);
+      r.full[slot].fetch_add(1, std::memory_order_release);
 #ifdef PLANT_PEEK_WRONG_SLOT
     seen = r.empty[slot].load(std::memory_order_acquire);
 #else
