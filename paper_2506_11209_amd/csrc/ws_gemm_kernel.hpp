@@ -185,6 +185,14 @@ constexpr bool swz_a_period32() {
 static_assert(swz_a_period32<32>() && swz_a_period32<64>() && swz_a_period32<128>(),
               "A swizzle must repeat every 32 rows and stay inside the row");
 
+// True when rows r and r + step of an A tile use the same swizzle for every r.
+template <int TK>
+constexpr bool swz_a_step_invariant(int step) {
+  for (int r = 0; r < 64; ++r)
+    if (swz_a<TK>(r + step) != swz_a<TK>(r)) return false;
+  return true;
+}
+
 __device__ __forceinline__ uint32_t lds_peek(WSG_LDS uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
@@ -507,6 +515,16 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc(const void* base) {
 constexpr int kBufferNonTemporal = 2;
 __device__ __forceinline__ i32x4_t panel_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
   return __builtin_bit_cast(i32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 0));
+}
+// The general variant's producers read through a resource whose record count
+// is 2^31 bytes.  Every chunk inside a panel lies below that (the plan keeps
+// panel offsets under 2^31), and a chunk outside A or B is read from offset
+// kOutsidePanel = 2^31: the range check of a raw buffer load returns zeros
+// for it without touching memory.
+constexpr uint32_t kOutsidePanel = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc_clipped(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)kOutsidePanel,
+                                           kRawBufferWord3);
 }
 // 16 bytes per lane straight into LDS: lane l's bytes land at dst + 16 l.
 __device__ __forceinline__ void panel_load16_lds(__amdgpu_buffer_rsrc_t r, WSG_LDS void* dst, uint32_t byte_off) {
@@ -875,7 +893,6 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
   constexpr int L1 = (63 / LOADS) < L0 ? (63 / LOADS) : L0;
   constexpr int L = L1 < 1 ? 1 : (L1 > 6 ? 6 : L1);  // K-iterations staged in VGPRs
   static_assert(G::A_INSTR % A_GROUP == 0 && G::B_INSTR % B_GROUP == 0, "even split");
-  static_assert(LOADS <= 32, "one validity bit per chunk");
 
   WSG_LDS uint32_t* full = (WSG_LDS uint32_t*)smem;
   WSG_LDS uint32_t* empty = full + kMaxStages;
@@ -895,6 +912,26 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
     const int blk = q >> 3, w = q & 7;
     const int kq = blk / G::NQ, nq = blk % G::NQ;
     goff[A_PER + n] = (uint32_t)((kq * 4 + (w >> 1)) * N + nq * 16 + (w & 1) * 8) * 2u;
+  }
+  // The general variant needs registers for its edge tests: where a wave's
+  // successive A (B) instructions lie a whole number of swizzle periods
+  // (block rows) apart, it keeps only the first instruction's offset, row
+  // and column and adds the (wave-uniform) step between instructions.
+  constexpr int A_STEP = (64 / G::CA) * A_GROUP;  // A rows from one of a wave's instructions to the next
+  constexpr bool kStrided = GENERAL && swz_a_step_invariant<TK>(A_STEP) && (8 * B_GROUP) % G::NQ == 0;
+  constexpr int B_STEP = (8 * B_GROUP) / G::NQ;   // B block rows (4 K rows each) between instructions
+  const uint32_t a_step = (uint32_t)A_STEP * (uint32_t)K * 2u;      // bytes, wave-uniform
+  const uint32_t b_step = (uint32_t)(B_STEP * 4) * (uint32_t)N * 2u;
+  // kStrided: the lane's first A row and K chunk, first B K row and column
+  int a_row0 = 0, a_kc0 = 0, b_kr0 = 0, b_nc0 = 0;
+  if constexpr (kStrided) {
+    const int qa = a_rank * 64 + lane;
+    a_row0 = qa / G::CA;
+    a_kc0 = 8 * ((qa % G::CA) ^ swz_a<TK>(a_row0));
+    const int qb = b_rank * 64 + lane;
+    const int blk = qb >> 3, w = qb & 7;
+    b_kr0 = (blk / G::NQ) * 4 + (w >> 1);
+    b_nc0 = (blk % G::NQ) * 16 + (w & 1) * 8;
   }
   const uint32_t lane16 = (uint32_t)lane * 16u;
 
@@ -918,12 +955,6 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
   // its slot, stands for the landing of q and the issue of q + L (the loads
   // go out right after q's signal).
   uint32_t t_issue[L], t_now = 0;
-  // GENERAL: bit n of vmask[u] says chunk n of staged iteration u lies inside
-  // A / B.  A chunk outside is fetched from the tile's first element (always
-  // inside) and written to LDS as zeros, so partial tiles and the tail of the
-  // last K-iteration contribute nothing.
-  uint32_t vmask[L];
-  uint32_t edge = 0;  // bit u: staged iteration u touches an edge of A or B (wave-uniform)
   // Loads go out unconditionally (past the last K-iteration they re-read the
   // last valid tile and are never written to LDS), so every path through the
   // loop has the same number of loads in flight and the compiler's vmcnt
@@ -932,43 +963,63 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
     if constexpr (tracing) t_issue[u] = t_now;
     const char* a_src = (const char*)(args.A + (int64_t)ti_i * TM * K + kk_i * TK);
     const char* b_src = (const char*)(args.B + (int64_t)kk_i * TK * N + (int64_t)tj_i * TN);
-    // GENERAL: a K-iteration whose tiles lie wholly inside A and B (the
-    // test is wave-uniform) loads as the plain kernel does; only the others
-    // mask their chunks.
-    bool interior = true;
+    // GENERAL: rows, columns and K left from this K-iteration's tile origin
+    // (wave-uniform; the origin is always inside A and B)
     int rows_left = 0, cols_left = 0, k_left = 0;
     if constexpr (GENERAL) {
       rows_left = args.M - ti_i * TM;
       cols_left = N - tj_i * TN;
       k_left = K - (int)kk_i * TK;
-      interior = rows_left >= TM && cols_left >= TN && k_left >= TK;
-      edge = (edge & ~(1u << u)) | ((interior ? 0u : 1u) << u);
     }
-    const __amdgpu_buffer_rsrc_t ra = panel_rsrc(a_src), rb = panel_rsrc(b_src);
-    if (GENERAL && !interior) {
+    const __amdgpu_buffer_rsrc_t ra = GENERAL ? panel_rsrc_clipped(a_src) : panel_rsrc(a_src);
+    const __amdgpu_buffer_rsrc_t rb = GENERAL ? panel_rsrc_clipped(b_src) : panel_rsrc(b_src);
+    if (GENERAL) {
       // K and N are multiples of 8, so a 16-byte chunk is wholly inside or
-      // wholly outside; the tile origin is always inside.
-      uint32_t m = 0;
+      // wholly outside A / B.  A chunk outside loads from kOutsidePanel,
+      // which the clipped resource's range check returns as zeros: partial
+      // tiles and the tail of the last K-iteration contribute nothing.  The
+      // test runs on every K-iteration, interior ones included: a branch
+      // between an interior and an edge form of these loads gives the
+      // compiler's wait-count analysis a path with fewer loads in flight,
+      // and it then waits for all of them before each slot write.
+      if constexpr (kStrided) {
+        // From the lane's first chunks and the steps.  The opaque copies
+        // keep the compiler from hoisting one offset per chunk out of the
+        // loop (they would not fit in the registers left).
+        uint32_t ab = goff[0], bb = goff[A_PER];
+        int ar = a_row0, bk = b_kr0;
+        asm volatile("" : "+v"(ab), "+v"(bb), "+v"(ar), "+v"(bk));
+        const bool a_kok = a_kc0 < k_left;
 #pragma unroll
-      for (int n = 0; n < A_PER; ++n) {
-        const int q = (a_rank + n * A_GROUP) * 64 + lane;
-        const int r = q / G::CA;
-        const int kc = 8 * ((q % G::CA) ^ swz_a<TK>(r));
-        const bool ok = r < rows_left && kc < k_left;
-        m |= (uint32_t)ok << n;
-        stage[u][n] = panel_load16(ra, ok ? goff[n] : 0u);
-      }
+        for (int n = 0; n < A_PER; ++n) {
+          const bool ok = a_kok && ar + n * A_STEP < rows_left;
+          stage[u][n] = panel_load16(ra, ok ? ab + (uint32_t)n * a_step : kOutsidePanel);
+        }
+        const bool b_cok = b_nc0 < cols_left;
 #pragma unroll
-      for (int n = 0; n < B_PER; ++n) {
-        const int q = (b_rank + n * B_GROUP) * 64 + lane;
-        const int blk = q >> 3, w = q & 7;
-        const int kr = (blk / G::NQ) * 4 + (w >> 1);
-        const int nc8 = (blk % G::NQ) * 16 + (w & 1) * 8;
-        const bool ok = kr < k_left && nc8 < cols_left;
-        m |= (uint32_t)ok << (A_PER + n);
-        stage[u][A_PER + n] = panel_load16(rb, ok ? goff[A_PER + n] : 0u);
+        for (int n = 0; n < B_PER; ++n) {
+          const bool ok = b_cok && bk + n * (B_STEP * 4) < k_left;
+          stage[u][A_PER + n] = panel_load16(rb, ok ? bb + (uint32_t)n * b_step : kOutsidePanel);
+        }
+      } else {
+#pragma unroll
+        for (int n = 0; n < A_PER; ++n) {
+          const int q = (a_rank + n * A_GROUP) * 64 + lane;
+          const int r = q / G::CA;
+          const int kc = 8 * ((q % G::CA) ^ swz_a<TK>(r));
+          const bool ok = r < rows_left && kc < k_left;
+          stage[u][n] = panel_load16(ra, ok ? goff[n] : kOutsidePanel);
+        }
+#pragma unroll
+        for (int n = 0; n < B_PER; ++n) {
+          const int q = (b_rank + n * B_GROUP) * 64 + lane;
+          const int blk = q >> 3, w = q & 7;
+          const int kr = (blk / G::NQ) * 4 + (w >> 1);
+          const int nc8 = (blk % G::NQ) * 16 + (w & 1) * 8;
+          const bool ok = kr < k_left && nc8 < cols_left;
+          stage[u][A_PER + n] = panel_load16(rb, ok ? goff[A_PER + n] : kOutsidePanel);
+        }
       }
-      vmask[u] = m;
     } else {
 #pragma unroll
       for (int n = 0; n < A_PER; ++n) stage[u][n] = panel_load16(ra, goff[n]);
@@ -1012,11 +1063,6 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
       debug_delay(args.producer_delay);
       compiler_fence();
       WSG_LDS char* base = smem + kHeaderBytes + slot * G::STAGE + lane16;
-      if (GENERAL && ((edge >> u) & 1u)) {
-#pragma unroll
-        for (int n = 0; n < LOADS; ++n)
-          if (!((vmask[u] >> n) & 1u)) stage[u][n] = i32x4_t{0, 0, 0, 0};
-      }
 #pragma unroll
       for (int n = 0; n < A_PER; ++n)
         *(WSG_LDS i32x4_t*)(base + (a_rank + n * A_GROUP) * 1024) = stage[u][n];
@@ -1700,11 +1746,13 @@ __global__ void __launch_bounds__((NC + NPW) * 64, (kernel_waves_per_simd<TM, TN
       consumer_release_only<G::NP, NC>(args, smem);
     } else if constexpr (MODE == kModeEpilogue) {
       consumer_epilogue_only<TM, TN, TK, NC, NPW, SPLIT, BF16>(args, wave, lane);
-    } else if constexpr (!GENERAL && (MODE == kModeGemm || MODE == kModeMath) &&
+    } else if constexpr ((!GENERAL || NC == 8) && (MODE == kModeGemm || MODE == kModeMath) &&
                          RollLoop<TM, TN, TK, NC, NPW, BF16>::kAvailable) {
       // Two consumer waves per SIMD (eight consumer waves, or four with two
       // workgroups per CU): the generated register-lean K loop (and its
-      // event-traced twin).
+      // event-traced twin).  The general variant of the eight-consumer
+      // arrangement runs it too: its producers zero-fill what lies outside A
+      // and B, so the K loop is the plain one, and only the epilogue differs.
       consumer_roll<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
     } else if constexpr (G::NW > 8 && G::BM * G::BN >= 8) {
       // Three waves per SIMD leave 168 VGPRs: the largest wave tiles then

@@ -31,6 +31,8 @@ LAUNCHES = [
     ((256, 512, 256), (256, 128, 64), 3, 8, 4, "bf16"),    # whole tiles, 2:1 (single-buffered consumer)
     ((129, 264, 200), (256, 128, 64), 3, 4, 4, "bf16"),    # partial tiles in M, N and K
     ((300, 136, 72), (64, 64, 32), 3, 2, 1, "f16"),        # partial tiles, one consumer wave, 2:1
+    ((512, 256, 192), (256, 256, 64), 2, 4, 8, "bf16"),    # whole tiles, eight consumer waves (roll loop)
+    ((300, 264, 200), (256, 256, 64), 2, 4, 8, "bf16"),    # partial tiles, eight consumer waves
 ]
 COEFFS = [(1.0, 0.0), (0.5, 0.0), (-2.0, 1.0), (0.5, -0.25), (0.0, 1.0)]
 

@@ -12,7 +12,8 @@ pytestmark = pytest.mark.gpu
 
 SHAPES = [(1, 8, 8), (7, 136, 72), (129, 264, 200), (300, 520, 4104), (257, 8, 4104), (1000, 1000, 1000)]
 CONFIGS = [((256, 128, 64), 3, 4, 4), ((128, 256, 32), 4, 8, 4), ((64, 64, 64), 3, 4, 4),
-           ((32, 32, 32), 2, 1, 1), ((64, 64, 32), 3, 2, 1), ((256, 128, 64), 3, 8, 4)]
+           ((32, 32, 32), 2, 1, 1), ((64, 64, 32), 3, 2, 1), ((256, 128, 64), 3, 8, 4),
+           ((256, 256, 64), 2, 4, 8)]
 GUARD = 4096
 SENTINEL = -7.0
 

@@ -205,9 +205,11 @@ def test_register_staged_producers_never_drain_their_staged_loads(library_code):
     flight and writes the oldest one to its slot: the wait before that write
     must leave the newer iterations' loads outstanding.  A wait for every
     load (vmcnt(0)) there empties the pipeline and exposes a full memory
-    latency; the compiler placed one at the first register stage of every
+    latency.  The compiler placed one at the first register stage of every
     pass through the stages while the wait loop could leave the loop early
-    (10 % of the load-only time at 16384 x 256 x 8192)."""
+    (10 % of the load-only time at 16384 x 256 x 8192), and before every
+    slot write of the general variant while its loads branched between an
+    interior and an edge form (8000^3 ran at a third of its speed)."""
     kernels, drained = 0, []
     for name, _, ins in library_code:
         if "ws_gemm_kernel" not in name:
