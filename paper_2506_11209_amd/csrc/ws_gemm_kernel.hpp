@@ -1758,11 +1758,11 @@ __global__ void __launch_bounds__((NC + NPW) * 64, (kernel_waves_per_simd<TM, TN
       // Three waves per SIMD leave 168 VGPRs: the largest wave tiles then
       // take the single-buffered consumer.
       consumer_rolling<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
-    } else if constexpr (!GENERAL && !TRACE && (MODE == kModeGemm || MODE == kModeMath) &&
+    } else if constexpr (!TRACE && (MODE == kModeGemm || MODE == kModeMath) &&
                          DeepLoop<TM, TN, TK, NC, NPW, BF16>::kAvailable) {
       // One producer group with the largest tiles (DeepLoop lists them): the
-      // hand-scheduled deep-prefetch K loop (measured slower than the
-      // compiler-scheduled loop in the general variant, so not used there).
+      // hand-scheduled deep-prefetch K loop, in the general variant too (its
+      // producers zero-fill what lies outside A and B).
       consumer_deep<TM, TN, TK, NC, NPW, SPLIT, BF16, MODE, GENERAL>(args, smem, wave, lane);
     } else {
       consumer<TM, TN, TK, NC, NPW, SPLIT, BF16, TRACE, MODE, GENERAL>(args, smem, wave, lane);
