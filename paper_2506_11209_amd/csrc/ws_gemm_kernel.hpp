@@ -526,6 +526,13 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc_clipped(const void*
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)kOutsidePanel,
                                            kRawBufferWord3);
 }
+// The same with the record count cut to the bytes from the panel base to the
+// end of the matrix (at most 2^31): a row-major panel's rows past the
+// matrix's last row then read as zeros too.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc_to_end(const void* base, int64_t bytes_left) {
+  const uint32_t n = bytes_left < (int64_t)kOutsidePanel ? (uint32_t)bytes_left : kOutsidePanel;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, kRawBufferWord3);
+}
 // 16 bytes per lane straight into LDS: lane l's bytes land at dst + 16 l.
 __device__ __forceinline__ void panel_load16_lds(__amdgpu_buffer_rsrc_t r, WSG_LDS void* dst, uint32_t byte_off) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, byte_off, 0, 0, 0);
@@ -915,23 +922,21 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
   }
   // The general variant needs registers for its edge tests: where a wave's
   // successive A (B) instructions lie a whole number of swizzle periods
-  // (block rows) apart, it keeps only the first instruction's offset, row
-  // and column and adds the (wave-uniform) step between instructions.
+  // (block rows) apart, it keeps only the first instruction's offset and
+  // adds the (wave-uniform) step between instructions.
   constexpr int A_STEP = (64 / G::CA) * A_GROUP;  // A rows from one of a wave's instructions to the next
   constexpr bool kStrided = GENERAL && swz_a_step_invariant<TK>(A_STEP) && (8 * B_GROUP) % G::NQ == 0;
   constexpr int B_STEP = (8 * B_GROUP) / G::NQ;   // B block rows (4 K rows each) between instructions
   const uint32_t a_step = (uint32_t)A_STEP * (uint32_t)K * 2u;      // bytes, wave-uniform
   const uint32_t b_step = (uint32_t)(B_STEP * 4) * (uint32_t)N * 2u;
-  // kStrided: the lane's first A row and K chunk, first B K row and column
-  int a_row0 = 0, a_kc0 = 0, b_kr0 = 0, b_nc0 = 0;
+  // kStrided: the lane's K chunk of A and column chunk of B (the same for
+  // all of its instructions)
+  int a_kc0 = 0, b_nc0 = 0;
   if constexpr (kStrided) {
     const int qa = a_rank * 64 + lane;
-    a_row0 = qa / G::CA;
-    a_kc0 = 8 * ((qa % G::CA) ^ swz_a<TK>(a_row0));
+    a_kc0 = 8 * ((qa % G::CA) ^ swz_a<TK>(qa / G::CA));
     const int qb = b_rank * 64 + lane;
-    const int blk = qb >> 3, w = qb & 7;
-    b_kr0 = (blk / G::NQ) * 4 + (w >> 1);
-    b_nc0 = (blk % G::NQ) * 16 + (w & 1) * 8;
+    b_nc0 = ((qb >> 3) % G::NQ) * 16 + (qb & 1) * 8;
   }
   const uint32_t lane16 = (uint32_t)lane * 16u;
 
@@ -971,8 +976,14 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
       cols_left = N - tj_i * TN;
       k_left = K - (int)kk_i * TK;
     }
-    const __amdgpu_buffer_rsrc_t ra = GENERAL ? panel_rsrc_clipped(a_src) : panel_rsrc(a_src);
-    const __amdgpu_buffer_rsrc_t rb = GENERAL ? panel_rsrc_clipped(b_src) : panel_rsrc(b_src);
+    // kStrided: the record counts end at the last row of A (the last K row
+    // of B); offsets stay 16-byte multiples, so no chunk straddles the end
+    const __amdgpu_buffer_rsrc_t ra =
+        kStrided ? panel_rsrc_to_end(a_src, ((int64_t)rows_left * K - (int64_t)kk_i * TK) * 2)
+                 : GENERAL ? panel_rsrc_clipped(a_src) : panel_rsrc(a_src);
+    const __amdgpu_buffer_rsrc_t rb =
+        kStrided ? panel_rsrc_to_end(b_src, ((int64_t)k_left * N - (int64_t)tj_i * TN) * 2)
+                 : GENERAL ? panel_rsrc_clipped(b_src) : panel_rsrc(b_src);
     if (GENERAL) {
       // K and N are multiples of 8, so a 16-byte chunk is wholly inside or
       // wholly outside A / B.  A chunk outside loads from kOutsidePanel,
@@ -983,24 +994,21 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
       // compiler's wait-count analysis a path with fewer loads in flight,
       // and it then waits for all of them before each slot write.
       if constexpr (kStrided) {
-        // From the lane's first chunks and the steps.  The opaque copies
+        // From the lane's first chunks and the steps.  Rows of A past M and
+        // K rows of B past K lie beyond the record counts; a lane whose
+        // K chunk of A (column chunk of B) is past K (N) starts at
+        // kOutsidePanel, and every chunk offset from there stays below 2^32
+        // (a step times the chunk index is below 2^31).  The opaque copies
         // keep the compiler from hoisting one offset per chunk out of the
         // loop (they would not fit in the registers left).
         uint32_t ab = goff[0], bb = goff[A_PER];
-        int ar = a_row0, bk = b_kr0;
-        asm volatile("" : "+v"(ab), "+v"(bb), "+v"(ar), "+v"(bk));
-        const bool a_kok = a_kc0 < k_left;
+        asm volatile("" : "+v"(ab), "+v"(bb));
+        ab = a_kc0 < k_left ? ab : kOutsidePanel;
+        bb = b_nc0 < cols_left ? bb : kOutsidePanel;
 #pragma unroll
-        for (int n = 0; n < A_PER; ++n) {
-          const bool ok = a_kok && ar + n * A_STEP < rows_left;
-          stage[u][n] = panel_load16(ra, ok ? ab + (uint32_t)n * a_step : kOutsidePanel);
-        }
-        const bool b_cok = b_nc0 < cols_left;
+        for (int n = 0; n < A_PER; ++n) stage[u][n] = panel_load16(ra, ab + (uint32_t)n * a_step);
 #pragma unroll
-        for (int n = 0; n < B_PER; ++n) {
-          const bool ok = b_cok && bk + n * (B_STEP * 4) < k_left;
-          stage[u][A_PER + n] = panel_load16(rb, ok ? bb + (uint32_t)n * b_step : kOutsidePanel);
-        }
+        for (int n = 0; n < B_PER; ++n) stage[u][A_PER + n] = panel_load16(rb, bb + (uint32_t)n * b_step);
       } else {
 #pragma unroll
         for (int n = 0; n < A_PER; ++n) {
