@@ -516,19 +516,15 @@ constexpr int kBufferNonTemporal = 2;
 __device__ __forceinline__ i32x4_t panel_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
   return __builtin_bit_cast(i32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 0));
 }
-// The general variant's producers read through a resource whose record count
-// is 2^31 bytes.  Every chunk inside a panel lies below that (the plan keeps
-// panel offsets under 2^31), and a chunk outside A or B is read from offset
-// kOutsidePanel = 2^31: the range check of a raw buffer load returns zeros
-// for it without touching memory.
+// The general variant's producers read through resources whose record count
+// ends at the end of the matrix (at most 2^31 bytes: the plan keeps panel
+// offsets under 2^31).  A chunk outside A or B lies past the record count or
+// is read from offset kOutsidePanel = 2^31; the range check of a raw buffer
+// load returns zeros for it without touching memory.
 constexpr uint32_t kOutsidePanel = 0x80000000u;
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc_clipped(const void* base) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)kOutsidePanel,
-                                           kRawBufferWord3);
-}
-// The same with the record count cut to the bytes from the panel base to the
-// end of the matrix (at most 2^31): a row-major panel's rows past the
-// matrix's last row then read as zeros too.
+// Record count: the bytes from the panel base to the end of the matrix, at
+// most 2^31; a row-major panel's rows past the matrix's last row read as
+// zeros.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc_to_end(const void* base, int64_t bytes_left) {
   const uint32_t n = bytes_left < (int64_t)kOutsidePanel ? (uint32_t)bytes_left : kOutsidePanel;
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, kRawBufferWord3);
@@ -976,28 +972,28 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
       cols_left = N - tj_i * TN;
       k_left = K - (int)kk_i * TK;
     }
-    // kStrided: the record counts end at the last row of A (the last K row
+    // GENERAL: the record counts end at the last row of A (the last K row
     // of B); offsets stay 16-byte multiples, so no chunk straddles the end
     const __amdgpu_buffer_rsrc_t ra =
-        kStrided ? panel_rsrc_to_end(a_src, ((int64_t)rows_left * K - (int64_t)kk_i * TK) * 2)
-                 : GENERAL ? panel_rsrc_clipped(a_src) : panel_rsrc(a_src);
+        GENERAL ? panel_rsrc_to_end(a_src, ((int64_t)rows_left * K - (int64_t)kk_i * TK) * 2)
+                : panel_rsrc(a_src);
     const __amdgpu_buffer_rsrc_t rb =
-        kStrided ? panel_rsrc_to_end(b_src, ((int64_t)k_left * N - (int64_t)tj_i * TN) * 2)
-                 : GENERAL ? panel_rsrc_clipped(b_src) : panel_rsrc(b_src);
+        GENERAL ? panel_rsrc_to_end(b_src, ((int64_t)k_left * N - (int64_t)tj_i * TN) * 2)
+                : panel_rsrc(b_src);
     if (GENERAL) {
       // K and N are multiples of 8, so a 16-byte chunk is wholly inside or
-      // wholly outside A / B.  A chunk outside loads from kOutsidePanel,
-      // which the clipped resource's range check returns as zeros: partial
-      // tiles and the tail of the last K-iteration contribute nothing.  The
-      // test runs on every K-iteration, interior ones included: a branch
+      // wholly outside A / B.  Rows of A past M and K rows of B past K lie
+      // beyond the record counts, and a chunk past K in A (past N in B)
+      // loads from kOutsidePanel; the range check returns zeros for both, so
+      // partial tiles and the tail of the last K-iteration contribute
+      // nothing.  The test runs on every K-iteration, interior ones included: a branch
       // between an interior and an edge form of these loads gives the
       // compiler's wait-count analysis a path with fewer loads in flight,
       // and it then waits for all of them before each slot write.
       if constexpr (kStrided) {
-        // From the lane's first chunks and the steps.  Rows of A past M and
-        // K rows of B past K lie beyond the record counts; a lane whose
-        // K chunk of A (column chunk of B) is past K (N) starts at
-        // kOutsidePanel, and every chunk offset from there stays below 2^32
+        // From the lane's first chunks and the steps.  A lane whose K chunk
+        // of A (column chunk of B) is past K (N) starts at kOutsidePanel,
+        // and every chunk offset from there stays below 2^32
         // (a step times the chunk index is below 2^31).  The opaque copies
         // keep the compiler from hoisting one offset per chunk out of the
         // loop (they would not fit in the registers left).
@@ -1013,19 +1009,14 @@ __device__ __forceinline__ void producer_loop_reg(const KernelArgs& args, WSG_LD
 #pragma unroll
         for (int n = 0; n < A_PER; ++n) {
           const int q = (a_rank + n * A_GROUP) * 64 + lane;
-          const int r = q / G::CA;
-          const int kc = 8 * ((q % G::CA) ^ swz_a<TK>(r));
-          const bool ok = r < rows_left && kc < k_left;
-          stage[u][n] = panel_load16(ra, ok ? goff[n] : kOutsidePanel);
+          const int kc = 8 * ((q % G::CA) ^ swz_a<TK>(q / G::CA));
+          stage[u][n] = panel_load16(ra, kc < k_left ? goff[n] : kOutsidePanel);
         }
 #pragma unroll
         for (int n = 0; n < B_PER; ++n) {
           const int q = (b_rank + n * B_GROUP) * 64 + lane;
-          const int blk = q >> 3, w = q & 7;
-          const int kr = (blk / G::NQ) * 4 + (w >> 1);
-          const int nc8 = (blk % G::NQ) * 16 + (w & 1) * 8;
-          const bool ok = kr < k_left && nc8 < cols_left;
-          stage[u][A_PER + n] = panel_load16(rb, ok ? goff[A_PER + n] : kOutsidePanel);
+          const int nc8 = ((q >> 3) % G::NQ) * 16 + (q & 1) * 8;
+          stage[u][A_PER + n] = panel_load16(rb, nc8 < cols_left ? goff[A_PER + n] : kOutsidePanel);
         }
       }
     } else {
